@@ -1,0 +1,147 @@
+"""CPU reference ("oracle") for the fused policy-loss path -- test infrastructure.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
+this package.  It shares no code with the HIP library and never imports it.
+The arithmetic lives in ``agrl_oracle.c`` (plain C: fp32 advantage
+normalisation in a fixed summation order, fp64 loss and gradients); this file
+only compiles it with gcc and marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_DIR = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_DIR, "agrl_oracle.c")
+_LIB = os.path.join(_DIR, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle (gcc, strict IEEE: no FMA contraction, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+                               "-fPIC", "-shared", "-pthread", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        _lib = ctypes.CDLL(_LIB)
+    return _lib
+
+
+def _p(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def _threads(n):
+    if n:
+        return int(n)
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def _as_input(x):
+    """numpy view of a torch/numpy matrix: (array, is_bf16)."""
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            x = x.detach().cpu().contiguous()
+            if x.dtype == torch.bfloat16:
+                return x.view(torch.int16).numpy().view(np.uint16), 1
+            return x.float().numpy(), 0
+    except ImportError:  # pragma: no cover
+        pass
+    x = np.ascontiguousarray(x)
+    if x.dtype == np.uint16:
+        return x, 1
+    return np.ascontiguousarray(x, np.float32), 0
+
+
+def task_adv_norm(traj_id, mask, traj_task, traj_group, reward, n_task, n_group=0, ddof=0,
+                  eps=1e-6):
+    lib = _load()
+    traj_id = np.ascontiguousarray(traj_id, np.int32)
+    mask = np.ascontiguousarray(mask, np.uint8)
+    traj_task = np.ascontiguousarray(traj_task, np.int32)
+    reward = np.ascontiguousarray(reward, np.float32)
+    if traj_group is not None:
+        traj_group = np.ascontiguousarray(traj_group, np.int32)
+    T_g, n_traj = traj_id.shape[0], traj_task.shape[0]
+    out = dict(act_count=np.zeros(n_traj, np.int32), task_count=np.zeros(n_task, np.int64),
+               task_mean=np.zeros(n_task, np.float32), task_std=np.zeros(n_task, np.float32),
+               adv_traj=np.zeros(n_traj, np.float32), adv_tok=np.zeros(T_g, np.float32))
+    f = lib.oracle_task_adv_norm
+    f.restype = ctypes.c_int
+    rc = f(ctypes.c_int64(T_g), ctypes.c_int32(n_traj), ctypes.c_int32(n_task),
+           ctypes.c_int32(n_group), _p(traj_id), _p(mask), _p(traj_task), _p(traj_group),
+           _p(reward), ctypes.c_int32(ddof), ctypes.c_float(eps), _p(out["act_count"]),
+           _p(out["task_count"]), _p(out["task_mean"]), _p(out["task_std"]),
+           _p(out["adv_traj"]), _p(out["adv_tok"]))
+    if rc != 0:
+        raise ValueError("oracle_task_adv_norm: id out of range")
+    return out
+
+
+def policy_loss(H, W, token_id, mask, adv, old_logp, eps_lo=0.2, eps_hi=0.2, n_norm=0,
+                temperature=1.0, grad_loss=1.0, backward=True, nthreads=None):
+    """Whole-batch forward (+ backward): logp, lse, loss, n_clip, g, dH, dW (fp64)."""
+    lib = _load()
+    Hn, hb = _as_input(H)
+    Wn, wb = _as_input(W)
+    assert hb == wb
+    T, d = Hn.shape
+    V = Wn.shape[0]
+    y = np.ascontiguousarray(token_id, np.int32)
+    m = np.ascontiguousarray(mask, np.uint8)
+    a = np.ascontiguousarray(adv, np.float32)
+    o = np.ascontiguousarray(old_logp, np.float32)
+    logp, lse, g = np.zeros(T), np.zeros(T), np.zeros(T)
+    loss = np.zeros(1)
+    n_clip = np.zeros(2, np.int64)
+    dH = np.zeros((T, d)) if backward else None
+    dW = np.zeros((V, d)) if backward else None
+    f = lib.oracle_policy_loss
+    f.restype = ctypes.c_int
+    rc = f(ctypes.c_int64(T), ctypes.c_int32(d), ctypes.c_int32(V), ctypes.c_int32(hb),
+           _p(Hn), _p(Wn), _p(y), _p(m), _p(a), _p(o), ctypes.c_double(eps_lo),
+           ctypes.c_double(eps_hi), ctypes.c_int64(n_norm), ctypes.c_double(temperature),
+           ctypes.c_double(grad_loss), ctypes.c_int(_threads(nthreads)), _p(logp), _p(lse),
+           _p(loss), _p(n_clip), _p(g), _p(dH), _p(dW))
+    if rc != 0:
+        raise ValueError("oracle_policy_loss: token id out of range")
+    return dict(logp=logp, lse=lse, loss=float(loss[0]), n_clip=n_clip, g=g, dH=dH, dW=dW)
+
+
+def token_sample(H, W, token_id, mask, adv, old_logp, tokens, eps_lo=0.2, eps_hi=0.2, n_norm=0,
+                 temperature=1.0, grad_loss=1.0, dH=True, nthreads=None):
+    """lse, logp, g and (optionally) the dH row for the listed token positions only."""
+    lib = _load()
+    Hn, hb = _as_input(H)
+    Wn, wb = _as_input(W)
+    assert hb == wb
+    T, d = Hn.shape
+    V = Wn.shape[0]
+    tok = np.ascontiguousarray(tokens, np.int64)
+    k = tok.shape[0]
+    lse, logp, g = np.zeros(k), np.zeros(k), np.zeros(k)
+    out_dH = np.zeros((k, d)) if dH else None
+    f = lib.oracle_token_sample
+    f.restype = ctypes.c_int
+    rc = f(ctypes.c_int64(T), ctypes.c_int32(d), ctypes.c_int32(V), ctypes.c_int32(hb),
+           _p(Hn), _p(Wn), _p(np.ascontiguousarray(token_id, np.int32)),
+           _p(np.ascontiguousarray(mask, np.uint8)), _p(np.ascontiguousarray(adv, np.float32)),
+           _p(np.ascontiguousarray(old_logp, np.float32)), ctypes.c_double(eps_lo),
+           ctypes.c_double(eps_hi), ctypes.c_int64(n_norm), ctypes.c_double(temperature),
+           ctypes.c_double(grad_loss), ctypes.c_int(_threads(nthreads)), _p(tok), ctypes.c_int64(k),
+           _p(lse), _p(logp), _p(g), _p(out_dH))
+    if rc != 0:
+        raise ValueError("oracle_token_sample: bad token index or id")
+    return dict(lse=lse, logp=logp, g=g, dH=out_dH)
