@@ -42,7 +42,7 @@ def test_golden_closed_forms(case):
         if key in exact:
             np.testing.assert_array_equal(got, want.astype(np.float32).astype(np.float64))
         else:
-            np.testing.assert_allclose(got, want, rtol=exp["rel"], atol=1e-12)
+            np.testing.assert_allclose(got, want, rtol=exp["rel"], atol=exp.get("atol", 1e-12))
 
 
 def _brute_counts(traj_id, mask, n_traj, traj_task, n_task):

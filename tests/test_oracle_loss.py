@@ -261,3 +261,34 @@ def test_config1_end_to_end_consistency():
     b = _brute(w.H.numpy(), w.W.numpy(), w.token_id, w.mask, adv, w.old_logp, 0.2, 0.2)
     assert r["loss"] == pytest.approx(b["loss"], rel=1e-10)
     np.testing.assert_allclose(r["dW"].sum(axis=0), 0.0, atol=1e-12)
+
+
+@pytest.mark.parametrize("eps", [(0.2, 0.28), (0.3, 0.2)])
+def test_decoupled_clip_bounds_hand_placed_ratios(eps):
+    """App. A (DAPO): clip(rho, 1 - eps_low, 1 + eps_high), bounds set independently.
+
+    Ratios are placed on both sides of every bound for A = +1 and A = -1; the
+    surrogate min(rho A, clip(rho) A) and which tokens stop the gradient follow
+    by hand: A > 0 is cut off only above 1 + eps_high, A < 0 only below 1 - eps_low.
+    """
+    lo, hi = eps
+    ratios = [1 - lo - 0.03, 1 - lo + 0.02, 0.95, 1.05, 1 + min(lo, hi) + 0.02,
+              1 + hi - 0.02, 1 + hi + 0.03, 1 + max(lo, hi) + 0.05]
+    rs = np.array(ratios * 2)
+    A = np.array([1.0] * len(ratios) + [-1.0] * len(ratios), np.float32)
+    T, V, d = len(rs), 9, 4
+    rng = np.random.default_rng(8)
+    H = rng.standard_normal((T, d)).astype(np.float32)
+    W = rng.standard_normal((V, d)).astype(np.float32)
+    y = rng.integers(0, V, T).astype(np.int32)
+    mask = np.ones(T, np.uint8)
+    lp = _brute(H, W, y, mask, A, np.zeros(T, np.float32), lo, hi)["logp"]
+    old = (lp - np.log(rs)).astype(np.float32)
+    rho = np.exp(lp - old.astype(np.float64))       # the fp32 rounding of old is carried
+    r = oracle.policy_loss(H, W, y, mask, A, old, eps_lo=lo, eps_hi=hi)
+    cut = ((A > 0) & (rho > 1 + hi)) | ((A < 0) & (rho < 1 - lo))
+    s = np.where(A > 0, np.minimum(rho, 1 + hi), -np.maximum(rho, 1 - lo))
+    assert r["loss"] == pytest.approx(-s.mean(), rel=1e-12)
+    assert list(r["n_clip"]) == [int(((A > 0) & (rho > 1 + hi)).sum()),
+                                 int(((A < 0) & (rho < 1 - lo)).sum())]
+    np.testing.assert_allclose(r["g"], np.where(cut, 0.0, -A * rho / T), rtol=1e-12, atol=0)
