@@ -1,0 +1,208 @@
+"""Throughput of the fused policy loss (forward + backward) on one MI355X.
+
+One step = the whole hot path over one batch: task advantage normalisation
+over the global batch of trajectories, then the fused LM-head / log-prob /
+clipped-surrogate forward and its backward (dH, dW) over the packed
+micro-batch.  Inputs are synthetic, drawn on the GPU before timing.
+
+Prints one JSON line.  ``value`` is packed micro-batch tokens per second;
+``mfma_frac`` is the executed matrix-core work of the step (four products of
+2 * N_act * V * d flops: forward logits, backward recompute, dW, dH) per
+second over the bf16 dense peak.  ``roofline`` describes the slowest of the
+four matrix-core launches, timed with HIP events on the library's stream.
+``cpu_baseline`` is the CPU oracle timed on a bounded sample of the same
+workload's action tokens on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15          # MI355X dense bf16 matrix-core peak, FLOP/s
+PEAK_F32 = 157.3e12
+HBM_PEAK = 8.0e12
+METRIC = "policy-loss fwd+bwd tokens/s and % of bf16 MFMA peak, 1 MI355X"
+PHASES = ["forward logits + lse", "backward logit recompute -> G", "dW = G^T H", "dH = G W"]
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (the library records them on its own stream)."""
+
+    def __init__(self, n: int):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            ev = ctypes.c_void_p()
+            rc = self.hip.hipEventCreate(ctypes.byref(ev))
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreate failed: {rc}")
+            self.arr[i] = ev
+
+    def slice_ptr(self, start: int):
+        return ctypes.cast(ctypes.byref(self.arr, start * ctypes.sizeof(ctypes.c_void_p)),
+                           ctypes.c_void_p).value
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), self.arr[a], self.arr[b])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return float(ms.value)
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, adv_tok_host, n_sample, n_act, T):
+    """The oracle's fwd+bwd on the first n_sample action tokens, scaled to the micro-batch."""
+    import oracle
+    act = np.nonzero(w.mask)[0][:n_sample]
+    H = w.H[torch.from_numpy(act).to(w.H.device)].cpu()
+    W = w.W.cpu()
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    t0 = time.perf_counter()
+    oracle.policy_loss(H, W, w.token_id[act], np.ones(len(act), np.uint8), adv_tok_host[act],
+                       w.old_logp[act], eps_lo=w.spec.eps_lo, eps_hi=w.spec.eps_hi,
+                       n_norm=n_act, nthreads=threads)
+    dt = time.perf_counter() - t0
+    per_token = dt / len(act)
+    return {"value": T / (per_token * n_act), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"fwd+bwd (logp, loss, dH, dW) of {len(act)} of the micro-batch's {n_act} "
+                      f"action tokens over the full V={w.V}, d={w.d} in fp64 took {dt:.2f} s on "
+                      f"{threads} threads; value = T / (time per action token * N_act)",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3, help="1..5; 3 is the 32B-shaped batch")
+    ap.add_argument("--cpu-tokens", type=int, default=32,
+                    help="action tokens in the oracle's timed sample (0 skips it)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the work would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2510_04206_amd as P
+    from paper_2510_04206_amd import _binding as B
+    from workloads import gen
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t0 = time.perf_counter()
+    w = gen.config(args.workload, device=dev)
+    log(f"workload {w.spec.name}: T={w.T} N_act={w.n_act} T_g={w.T_g} n_traj={w.n_traj} "
+        f"(generated in {time.perf_counter() - t0:.1f} s)")
+    V, d, T, n_act = w.V, w.d, w.T, w.n_act
+    dtype = w.H.dtype
+    code = P.AGRL_BF16 if dtype == torch.bfloat16 else P.AGRL_F32
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    g_traj, g_mask = t(w.g_traj_id), t(w.g_mask)
+    traj_task, traj_group, reward = t(w.traj_task), t(w.traj_group), t(w.reward)
+    token_id, mask, old = t(w.token_id), t(w.mask), t(w.old_logp)
+    H, W = w.H, w.W
+
+    n_traj, n_task = w.n_traj, w.n_task
+    act_count = torch.empty(n_traj, dtype=torch.int32, device=dev)
+    task_count = torch.empty(n_task, dtype=torch.int64, device=dev)
+    task_mean = torch.empty(n_task, dtype=torch.float32, device=dev)
+    task_std = torch.empty(n_task, dtype=torch.float32, device=dev)
+    adv_traj = torch.empty(n_traj, dtype=torch.float32, device=dev)
+    adv_tok = torch.empty(w.T_g, dtype=torch.float32, device=dev)
+    adv_mb = adv_tok[:T]        # the micro-batch is the global stream's first T tokens
+
+    K, Wm = args.steps, args.warmup
+    events = HipEvents(8 * (K + Wm))
+    opt = B.agrl_options()
+    pl = P.PolicyLoss(T, d, V, dtype, max_act=n_act, eps_low=w.spec.eps_lo,
+                      eps_high=w.spec.eps_hi, opt=opt, device=dev)
+    log(f"workspace {pl.ws_bytes / 2**30:.2f} GiB")
+
+    def step(i):
+        opt.phase_events = events.slice_ptr(8 * i)
+        B.agrl_task_adv_norm(w.T_g, n_traj, n_task, w.n_group, g_traj, g_mask, traj_task,
+                             traj_group, reward, None, act_count, task_count, task_mean,
+                             task_std, adv_traj, adv_tok)
+        pl.forward(H, W, token_id, mask, adv_mb, old)
+        pl.backward(H, W, token_id, mask, adv_mb, old)
+
+    for i in range(Wm):
+        step(i)
+    torch.cuda.synchronize()
+    if P.agrl_get_device_error() != 0:
+        raise RuntimeError("device error flag set during warm-up")
+    log(f"warm-up done; loss {pl.loss.item():.6g}")
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(Wm, Wm + K):
+        step(i)
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms = total_ms / K
+    if P.agrl_get_device_error() != 0:
+        raise RuntimeError("device error flag set during timing")
+
+    gemm_flops = 2.0 * n_act * V * d
+    phase_ms = [float(np.mean([events.elapsed_ms(8 * i + 2 * p, 8 * i + 2 * p + 1)
+                               for i in range(Wm, Wm + K)])) for p in range(4)]
+    peak = PEAK_BF16 if code == P.AGRL_BF16 else PEAK_F32
+    dom = int(np.argmax(phase_ms))
+    achieved = gemm_flops / (phase_ms[dom] * 1e-3)
+    step_flops = 4 * gemm_flops
+    log("phases (ms): " + ", ".join(f"{n}: {m:.3f}" for n, m in zip(PHASES, phase_ms)))
+
+    out = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if code == P.AGRL_BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.spec.name, "T": T, "N_act": n_act, "V": V, "d": d,
+                   "T_g": w.T_g, "n_traj": n_traj, "n_task": n_task},
+        "action_tokens_per_s": n_act / (ms * 1e-3),
+        "mfma_tflops": step_flops / (ms * 1e-3) / 1e12,
+        "mfma_frac": step_flops / (ms * 1e-3) / peak,
+        "gemm_ms": dict(zip(["fwd", "recompute", "dW", "dH"], phase_ms)),
+        "roofline": {"kernel": f"gemm_nt_kernel ({PHASES[dom]})", "bound": "mfma",
+                     "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "flops_per_launch": gemm_flops},
+    }
+    if args.cpu_tokens > 0:
+        adv_host = adv_tok[:T].cpu().numpy()
+        log(f"timing the oracle on {args.cpu_tokens} action tokens ...")
+        out["cpu_baseline"] = cpu_baseline(w, adv_host, args.cpu_tokens, n_act, T)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

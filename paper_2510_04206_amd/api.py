@@ -1,0 +1,68 @@
+"""Convenience layer over the C ABI: allocates outputs/workspace with torch, then calls it."""
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+
+from . import _binding as B
+
+
+def task_adv_norm(traj_id: torch.Tensor, action_mask: torch.Tensor, traj_task: torch.Tensor,
+                  traj_group: Optional[torch.Tensor], reward: torch.Tensor, n_task: int,
+                  n_group: int = 0, opt=None, with_tokens: bool = True, stream=None) -> dict:
+    """agrl_task_adv_norm on device tensors; returns the outputs as a dict."""
+    dev = traj_id.device
+    T_g, n_traj = traj_id.numel(), traj_task.numel()
+    out = dict(act_count=torch.empty(n_traj, dtype=torch.int32, device=dev),
+               task_count=torch.empty(n_task, dtype=torch.int64, device=dev),
+               task_mean=torch.empty(n_task, dtype=torch.float32, device=dev),
+               task_std=torch.empty(n_task, dtype=torch.float32, device=dev),
+               adv_traj=torch.empty(n_traj, dtype=torch.float32, device=dev),
+               adv_tok=torch.empty(T_g, dtype=torch.float32, device=dev) if with_tokens else None)
+    B.agrl_task_adv_norm(T_g, n_traj, n_task, n_group, traj_id, action_mask, traj_task,
+                         traj_group, reward, opt, out["act_count"], out["task_count"],
+                         out["task_mean"], out["task_std"], out["adv_traj"], out["adv_tok"],
+                         stream)
+    return out
+
+
+class PolicyLoss:
+    """Forward/backward of the fused policy loss for one micro-batch shape.
+
+    Holds the workspace (sized for T tokens with at most max_act action
+    tokens) and the output buffers, so repeated steps allocate nothing.
+    """
+
+    def __init__(self, T: int, d: int, V: int, dtype: torch.dtype, max_act: int = 0,
+                 eps_low: float = 0.2, eps_high: float = 0.2, n_norm: int = 0, opt=None,
+                 device="cuda"):
+        self.T, self.d, self.V, self.max_act = int(T), int(d), int(V), int(max_act)
+        self.code = B.AGRL_BF16 if dtype == torch.bfloat16 else B.AGRL_F32
+        self.eps_low, self.eps_high, self.n_norm = float(eps_low), float(eps_high), int(n_norm)
+        self.opt = B.agrl_options(**opt) if isinstance(opt, dict) else opt
+        self.ws_bytes = B.agrl_policy_loss_workspace_size(self.T, self.max_act, self.d, self.V,
+                                                          self.code, self.opt)
+        dev = torch.device(device)
+        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self.loss = torch.empty(1, dtype=torch.float32, device=dev)
+        self.logp = torch.empty(self.T, dtype=torch.float32, device=dev)
+        self.lse = torch.empty(self.T, dtype=torch.float32, device=dev)
+        self.n_clip = torch.empty(2, dtype=torch.int64, device=dev)
+        self.dH = torch.empty((self.T, self.d), dtype=torch.float32, device=dev)
+        self.dW = torch.empty((self.V, self.d), dtype=torch.float32, device=dev)
+
+    def forward(self, H, W, token_id, action_mask, adv_tok, old_logp, stream=None):
+        B.agrl_policy_loss_fwd(self.T, self.max_act, self.d, self.V, self.code, H, W, token_id,
+                               action_mask, adv_tok, old_logp, self.eps_low, self.eps_high,
+                               self.n_norm, self.opt, self.workspace, self.ws_bytes, self.loss,
+                               self.logp, self.lse, self.n_clip, stream)
+        return self.loss, self.logp, self.lse, self.n_clip
+
+    def backward(self, H, W, token_id, action_mask, adv_tok, old_logp, grad_loss: float = 1.0,
+                 stream=None):
+        B.agrl_policy_loss_bwd(self.T, self.max_act, self.d, self.V, self.code, H, W, token_id,
+                               action_mask, adv_tok, old_logp, self.eps_low, self.eps_high,
+                               self.n_norm, self.opt, self.lse, self.logp, float(grad_loss),
+                               self.workspace, self.ws_bytes, self.dH, self.dW, stream)
+        return self.dH, self.dW

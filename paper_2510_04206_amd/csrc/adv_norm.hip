@@ -1,0 +1,238 @@
+// Task advantage normalisation (AgentRL Sec. 3.2) on top of GRPO's group-relative
+// advantage (App. B.2), for a global batch of trajectories.
+//
+// Compiled with -ffp-contract=off: every + - * / and sqrtf below is one correctly
+// rounded fp32 operation, so the results are bit-identical to any implementation
+// that follows the same summation order (see agrl.h).
+#include <math.h>
+
+#include "../../include/agrl.h"
+#include "common.hpp"
+
+namespace agrl {
+namespace {
+
+constexpr int kCountPerLane = 16;
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// n_tau: each lane walks kCountPerLane consecutive tokens, adding runs of the
+// same trajectory; the wave then merges lanes that end on the same trajectory.
+// Integer atomics are exact, so the counts do not depend on the order.
+__global__ __launch_bounds__(256) void count_kernel(int64_t T_g, int32_t n_traj,
+                                                    const int32_t* __restrict__ traj_id,
+                                                    const uint8_t* __restrict__ mask,
+                                                    int32_t* act_count, int* err) {
+  const int64_t t0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kCountPerLane;
+  int cur = -1, cnt = 0;
+  for (int i = 0; i < kCountPerLane; ++i) {
+    const int64_t t = t0 + i;
+    if (t >= T_g) break;
+    const int id = traj_id[t];
+    if (id >= n_traj) {
+      set_error(err, ERR_TRAJ_ID);
+      continue;
+    }
+    if (id < 0 || !mask[t]) continue;
+    if (id != cur) {
+      if (cnt) atomicAdd(&act_count[cur], cnt);
+      cur = id;
+      cnt = 0;
+    }
+    ++cnt;
+  }
+  const int lane = threadIdx.x & 63;
+  for (;;) {
+    const uint64_t pend = __ballot(cnt > 0);
+    if (!pend) break;
+    const int leader = __ffsll((unsigned long long)pend) - 1;
+    const int lid = __shfl(cur, leader);
+    int mine = (cnt > 0 && cur == lid) ? cnt : 0;
+    for (int o = 32; o >= 1; o >>= 1) mine += __shfl_xor(mine, o);
+    if (lane == leader) atomicAdd(&act_count[lid], mine);
+    if (cnt > 0 && cur == lid) cnt = 0;
+  }
+}
+
+__global__ void check_ids_kernel(int32_t n_traj, int32_t n_task, int32_t n_group,
+                                 const int32_t* traj_task, const int32_t* traj_group, int* err) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n_traj) return;
+  if (traj_task[j] < 0 || traj_task[j] >= n_task) set_error(err, ERR_TASK_ID);
+  if (traj_group && (traj_group[j] < 0 || traj_group[j] >= n_group)) set_error(err, ERR_GROUP_ID);
+}
+
+// The fixed combination of a wave's 64 partial sums: acc_l += acc_{l xor o},
+// o = 32 .. 1.  All lanes end with the same bits.
+__device__ __forceinline__ float butterfly_sum(float acc) {
+  for (int o = 32; o >= 1; o >>= 1) acc = acc + __shfl_xor(acc, o);
+  return acc;
+}
+
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// GRPO stage: one wave per group.  Lane l owns trajectories l, l+64, ...
+__global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_traj,
+                                                    const int32_t* __restrict__ traj_group,
+                                                    const float* __restrict__ reward,
+                                                    int32_t ddof, float eps, float* a_hat) {
+  const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (g >= n_group) return;
+  const int lane = threadIdx.x & 63;
+  float acc = 0.0f;
+  int K = 0;
+  for (int base = 0; base < n_traj; base += 64) {
+    const int tau = base + lane;
+    const bool mem = tau < n_traj && traj_group[tau] == g;
+    if (mem) acc = acc + reward[tau];
+    K += __popcll(__ballot(mem));
+  }
+  if (K == 0) return;
+  if (K - ddof <= 0) {
+    for (int tau = lane; tau < n_traj; tau += 64)
+      if (traj_group[tau] == g) a_hat[tau] = 0.0f;
+    return;
+  }
+  const float mu = butterfly_sum(acc) / (float)K;
+  acc = 0.0f;
+  for (int tau = lane; tau < n_traj; tau += 64) {
+    if (traj_group[tau] == g) {
+      const float dv = reward[tau] - mu;
+      acc = acc + dv * dv;
+    }
+  }
+  const float var = butterfly_sum(acc) / (float)(K - ddof);
+  const float den = sqrtf(var) + eps;
+  for (int tau = lane; tau < n_traj; tau += 64)
+    if (traj_group[tau] == g) a_hat[tau] = (reward[tau] - mu) / den;
+}
+
+// Task stage: one wave per task; statistics of the token-level set, where
+// trajectory tau contributes its advantage with multiplicity n_tau.
+// src may alias adv_traj: each lane reads its own trajectories before writing them.
+__global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_traj,
+                                                   const int32_t* __restrict__ traj_task,
+                                                   const int32_t* __restrict__ act_count,
+                                                   const float* src, int32_t ddof, float eps,
+                                                   int64_t* task_count, float* task_mean,
+                                                   float* task_std, float* adv_traj) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= n_task) return;
+  const int lane = threadIdx.x & 63;
+  float acc = 0.0f;
+  int64_t n_lane = 0;
+  for (int tau = lane; tau < n_traj; tau += 64) {
+    if (traj_task[tau] == i) {
+      const int n = act_count[tau];
+      n_lane += n;
+      acc = acc + (float)n * src[tau];
+    }
+  }
+  const int64_t N = wave_sum_i64(n_lane);
+  if (N == 0) {
+    for (int tau = lane; tau < n_traj; tau += 64)
+      if (traj_task[tau] == i) adv_traj[tau] = 0.0f;
+    if (lane == 0) {
+      task_count[i] = 0;
+      task_mean[i] = 0.0f;
+      task_std[i] = 0.0f;
+    }
+    return;
+  }
+  const float mu = butterfly_sum(acc) / (float)N;
+  acc = 0.0f;
+  for (int tau = lane; tau < n_traj; tau += 64) {
+    if (traj_task[tau] == i) {
+      const float dv = src[tau] - mu;
+      acc = acc + (float)act_count[tau] * (dv * dv);
+    }
+  }
+  const float q = butterfly_sum(acc);
+  const float sigma = (N - ddof > 0) ? sqrtf(q / (float)(N - ddof)) : 0.0f;
+  const float den = sigma + eps;
+  for (int tau = lane; tau < n_traj; tau += 64)
+    if (traj_task[tau] == i) adv_traj[tau] = (src[tau] - mu) / den;
+  if (lane == 0) {
+    task_count[i] = N;
+    task_mean[i] = mu;
+    task_std[i] = sigma;
+  }
+}
+
+__global__ void broadcast_kernel(int64_t T_g, int32_t n_traj, const int32_t* __restrict__ traj_id,
+                                 const uint8_t* __restrict__ mask,
+                                 const float* __restrict__ adv_traj, float* adv_tok) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T_g) return;
+  const int id = traj_id[t];
+  adv_tok[t] = (mask[t] && id >= 0 && id < n_traj) ? adv_traj[id] : 0.0f;
+}
+
+int fail(int code, const char* msg) {
+  set_last_error(msg);
+  return code;
+}
+
+}  // namespace
+}  // namespace agrl
+
+extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_group,
+                                  const int32_t* traj_id, const uint8_t* action_mask,
+                                  const int32_t* traj_task, const int32_t* traj_group,
+                                  const float* reward, const agrl_options* opt,
+                                  int32_t* act_count, int64_t* task_count, float* task_mean,
+                                  float* task_std, float* adv_traj, float* adv_tok,
+                                  void* stream) {
+  using namespace agrl;
+  if (T_g < 0 || n_traj < 0 || n_task < 0 || n_group < 0)
+    return fail(AGRL_E_SHAPE, "agrl_task_adv_norm: negative size");
+  if (T_g > ((int64_t)1 << 40)) return fail(AGRL_E_SHAPE, "agrl_task_adv_norm: T_g too large");
+  if (traj_group && n_traj > 0 && n_group == 0)
+    return fail(AGRL_E_SHAPE, "agrl_task_adv_norm: traj_group given with n_group == 0");
+  if (T_g > 0 && (!traj_id || !action_mask))
+    return fail(AGRL_E_NULL, "agrl_task_adv_norm: traj_id/action_mask is NULL");
+  if (n_traj > 0 && (!traj_task || !reward || !act_count || !adv_traj))
+    return fail(AGRL_E_NULL, "agrl_task_adv_norm: per-trajectory array is NULL");
+  if (n_task > 0 && (!task_count || !task_mean || !task_std))
+    return fail(AGRL_E_NULL, "agrl_task_adv_norm: per-task output is NULL");
+  agrl_options o = {};
+  if (opt) o = *opt;
+  if (o.std_ddof != 0 && o.std_ddof != 1)
+    return fail(AGRL_E_FLAGS, "agrl_task_adv_norm: std_ddof must be 0 or 1");
+  if (!(o.std_eps >= 0.0f) || !isfinite(o.std_eps))
+    return fail(AGRL_E_FLAGS, "agrl_task_adv_norm: std_eps must be finite and >= 0");
+  const float eps = o.std_eps == 0.0f ? 1e-6f : o.std_eps;
+
+  hipStream_t s = (hipStream_t)stream;
+  int* err = device_error_ptr();
+  if (!err) return hip_status(hipErrorInvalidSymbol);
+
+  if (n_traj > 0) {
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, act_count,
+                       (int64_t)n_traj, 0);
+    hipLaunchKernelGGL(check_ids_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, n_traj,
+                       n_task, n_group, traj_task, traj_group, err);
+  }
+  if (T_g > 0 && n_traj >= 0) {
+    const int64_t lanes = cdiv<int64_t>(T_g, kCountPerLane);
+    hipLaunchKernelGGL(count_kernel, dim3((unsigned)cdiv<int64_t>(lanes, 256)), dim3(256), 0, s,
+                       T_g, n_traj, traj_id, action_mask, act_count, err);
+  }
+  if (traj_group && n_group > 0)
+    hipLaunchKernelGGL(group_kernel, dim3(cdiv(n_group, 4)), dim3(256), 0, s, n_group, n_traj,
+                       traj_group, reward, (int32_t)o.std_ddof, eps, adv_traj);
+  if (n_task > 0)
+    hipLaunchKernelGGL(task_kernel, dim3(cdiv(n_task, 4)), dim3(256), 0, s, n_task, n_traj,
+                       traj_task, act_count, traj_group ? (const float*)adv_traj : reward,
+                       (int32_t)o.std_ddof, eps, task_count, task_mean, task_std, adv_traj);
+  if (adv_tok && T_g > 0)
+    hipLaunchKernelGGL(broadcast_kernel, dim3((unsigned)cdiv<int64_t>(T_g, 256)), dim3(256), 0, s,
+                       T_g, n_traj, traj_id, action_mask, (const float*)adv_traj, adv_tok);
+  return hip_status(hipGetLastError());
+}

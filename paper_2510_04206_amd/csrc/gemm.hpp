@@ -1,0 +1,386 @@
+// Persistent "NT" GEMM on the gfx950 matrix cores: C[M, N] = A[M, K] * B[N, K]^T,
+// both operands K-contiguous, fp32 accumulation, with a fused epilogue functor.
+//
+// Block tile 256 x 256, 4 waves in a 2 x 2 arrangement, each wave owning a
+// 128 x 128 sub-tile as 4 x 4 blocks of 32 x 32 MFMA accumulators
+// (v_mfma_f32_32x32x16_bf16 for bf16, v_mfma_f32_32x32x2_f32 for fp32).
+// Each K stage moves 128 bytes of every tile row (64 bf16 or 32 fp32) through
+// LDS, double-buffered with one barrier per stage; 16-byte chunks are stored
+// at chunk ^ (row & 7) so that both the row-wise writes and the 32-row
+// fragment reads are free of bank conflicts.
+//
+// The grid is persistent (about one workgroup per compute unit, since a block
+// holds 128 KiB of LDS).  The row count M and the K extent may be read from
+// device memory, so a launch sized for an upper bound does only the work the
+// data needs without a host round trip.  Tile order: workgroups are dealt to
+// the 8 XCDs round-robin, so each full round of tiles is renumbered to give
+// every XCD a contiguous run, and runs are laid out group_m row-tiles deep so
+// the 32 workgroups of an XCD share A and B panels in its L2.
+#pragma once
+#include "common.hpp"
+
+namespace agrl {
+
+constexpr int GBM = 256;
+constexpr int GBN = 256;
+constexpr int LDS_ROW = 128;                            // bytes per tile row per stage
+constexpr int STAGE_BYTES = (GBM + GBN) * LDS_ROW;      // 64 KiB
+constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB
+constexpr int GEMM_THREADS = 256;
+
+template <typename T>
+struct KStage;
+template <>
+struct KStage<__bf16> {
+  static constexpr int BK = 64;
+};
+template <>
+struct KStage<float> {
+  static constexpr int BK = 32;
+};
+
+struct GemmShape {
+  const void* A;
+  int64_t lda;             // elements
+  const void* B;
+  int64_t ldb;
+  int32_t M;               // rows of A (used when m_dev == nullptr)
+  const int32_t* m_dev;    // rows of A read on the device
+  int32_t N;               // rows of B
+  int32_t K;               // multiple of BK (used when k_dev == nullptr)
+  const int32_t* k_dev;    // K read on the device, rounded up to BK
+  int32_t group_m;         // row-tiles per tile-order group
+};
+
+// Accumulator element (i, j, r) of a wave sits at
+//   row = wm*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4,  col = wn*128 + j*32 + lane%32.
+__device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
+  return wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+__device__ __forceinline__ int acc_col(int wn, int j, int lane) {
+  return wn * 128 + j * 32 + (lane & 31);
+}
+
+__device__ __forceinline__ void map_tile(int t, int grid, int total, int tiles_m, int tiles_n,
+                                         int group_m, int& tm, int& tn) {
+  int L = t;
+  const int round = t / grid;
+  if ((grid & 7) == 0 && (round + 1) * grid <= total) {
+    const int b = t - round * grid;
+    L = round * grid + (b & 7) * (grid >> 3) + (b >> 3);
+  }
+  const int width = group_m * tiles_n;
+  const int grp = L / width;
+  const int first = grp * group_m;
+  const int gsz = min(tiles_m - first, group_m);
+  const int rem = L - grp * width;
+  tm = first + rem % gsz;
+  tn = rem / gsz;
+}
+
+// One K stage of global loads: 8 16-byte chunks of A and of B per thread.
+__device__ __forceinline__ void load_stage(u32x4 (&ra)[8], u32x4 (&rb)[8], const uint8_t* A,
+                                           int64_t lda_b, int m0, int M, const uint8_t* B,
+                                           int64_t ldb_b, int n0, int N, int64_t k0_b, int tid) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int q = tid + GEMM_THREADS * i;
+    const int r = q >> 3, c = q & 7;
+    const int64_t ra_row = min(m0 + r, M - 1);
+    const int64_t rb_row = min(n0 + r, N - 1);
+    ra[i] = *(const u32x4*)(A + ra_row * lda_b + k0_b + c * 16);
+    rb[i] = *(const u32x4*)(B + rb_row * ldb_b + k0_b + c * 16);
+  }
+}
+
+__device__ __forceinline__ void store_stage(uint8_t* st, const u32x4 (&ra)[8],
+                                            const u32x4 (&rb)[8], int tid) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int q = tid + GEMM_THREADS * i;
+    const int r = q >> 3, c = q & 7;
+    const int off = r * LDS_ROW + ((c ^ (r & 7)) << 4);
+    *(u32x4*)(st + off) = ra[i];
+    *(u32x4*)(st + GBM * LDS_ROW + off) = rb[i];
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void compute_stage(const uint8_t* st, f32x16 (&acc)[4][4], int wm,
+                                              int wn, int lane);
+
+template <>
+__device__ __forceinline__ void compute_stage<__bf16>(const uint8_t* st, f32x16 (&acc)[4][4],
+                                                      int wm, int wn, int lane) {
+  const int sw = lane & 7;
+  const uint8_t* As = st + (wm * 128 + (lane & 31)) * LDS_ROW;
+  const uint8_t* Bs = st + GBM * LDS_ROW + (wn * 128 + (lane & 31)) * LDS_ROW;
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int chunk = ((kk * 2 + (lane >> 5)) ^ sw) << 4;
+    bf16x8 a[4], b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(As + i * 32 * LDS_ROW + chunk);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + j * 32 * LDS_ROW + chunk);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  }
+}
+
+template <>
+__device__ __forceinline__ void compute_stage<float>(const uint8_t* st, f32x16 (&acc)[4][4],
+                                                     int wm, int wn, int lane) {
+  const int sw = lane & 7;
+  const uint8_t* As = st + (wm * 128 + (lane & 31)) * LDS_ROW;
+  const uint8_t* Bs = st + GBM * LDS_ROW + (wn * 128 + (lane & 31)) * LDS_ROW;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int c0 = ((kk * 4 + (lane >> 5) * 2) ^ sw) << 4;
+    const int c1 = ((kk * 4 + (lane >> 5) * 2 + 1) ^ sw) << 4;
+    f32x4 a[4][2], b[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i][0] = *(const f32x4*)(As + i * 32 * LDS_ROW + c0);
+      a[i][1] = *(const f32x4*)(As + i * 32 * LDS_ROW + c1);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      b[j][0] = *(const f32x4*)(Bs + j * 32 * LDS_ROW + c0);
+      b[j][1] = *(const f32x4*)(Bs + j * 32 * LDS_ROW + c1);
+    }
+    // Lane l holds k = (l/32)*8 + e of this 16-wide slice in element e; MFMA e
+    // pairs element e of both operands, so the 8 MFMAs cover all 16 k once.
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e >> 2][e & 3], b[j][e >> 2][e & 3],
+                                                           acc[i][j], 0, 0, 0);
+  }
+}
+
+template <typename T, class Epi>
+__global__ void __launch_bounds__(GEMM_THREADS)
+    __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_nt_kernel(GemmShape g, Epi epi) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[GEMM_LDS];
+  constexpr int BK = KStage<T>::BK;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int M = g.m_dev ? *g.m_dev : g.M;
+  const int K = g.k_dev ? cdiv(*g.k_dev, BK) * BK : g.K;
+  if (M <= 0 || g.N <= 0) return;
+  const int tiles_m = cdiv(M, GBM), tiles_n = cdiv(g.N, GBN);
+  const int total = tiles_m * tiles_n;
+  const int nk = K / BK;
+  const uint8_t* A = (const uint8_t*)g.A;
+  const uint8_t* B = (const uint8_t*)g.B;
+  const int64_t lda_b = g.lda * (int64_t)sizeof(T), ldb_b = g.ldb * (int64_t)sizeof(T);
+
+  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+    int tm, tn;
+    map_tile(t, gridDim.x, total, tiles_m, tiles_n, g.group_m, tm, tn);
+    const int m0 = tm * GBM, n0 = tn * GBN;
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    if (nk > 0) {
+      u32x4 ra[8], rb[8];
+      load_stage(ra, rb, A, lda_b, m0, M, B, ldb_b, n0, g.N, 0, tid);
+      store_stage(smem, ra, rb, tid);
+      __syncthreads();
+      for (int kt = 0; kt < nk; ++kt) {
+        const uint8_t* cur = smem + (kt & 1) * STAGE_BYTES;
+        const bool more = kt + 1 < nk;
+        if (more)
+          load_stage(ra, rb, A, lda_b, m0, M, B, ldb_b, n0, g.N,
+                     (int64_t)(kt + 1) * BK * (int64_t)sizeof(T), tid);
+        compute_stage<T>(cur, acc, wm, wn, lane);
+        if (more) store_stage(smem + ((kt + 1) & 1) * STAGE_BYTES, ra, rb, tid);
+        __syncthreads();
+      }
+    }
+    epi(acc, m0, n0, tn, M, g.N, smem, wm, wn, lane, tid);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Epilogues.  Each receives the finished accumulators of one tile.
+
+// Forward: per row of the tile, the max and the sum of exp(z - max) over the
+// tile's vocabulary columns (z = acc / temperature), plus the target logit.
+struct EpiLsePartial {
+  const int32_t* y;      // [rows] target id of each compacted row
+  f32x2* part;           // [tiles_n][ld_part] (max, sum exp) per row and vocabulary tile
+  int64_t ld_part;
+  float* zy;             // [rows] logit of the target token
+  float scale;           // 1 / temperature
+
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                             int N, uint8_t* smem, int wm, int wn, int lane,
+                                             int tid) const {
+    int* sy = (int*)smem;
+    f32x2* red = (f32x2*)(smem + 1024);
+    sy[tid] = (m0 + tid < M) ? y[m0 + tid] : -1;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = acc_row(wm, i, r, lane);
+        const int target = sy[rl];
+        float v[4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = n0 + acc_col(wn, j, lane);
+          v[j] = c < N ? acc[i][j][r] * scale : -INFINITY;
+          mx = fmaxf(mx, v[j]);
+          if (c == target) zy[m0 + rl] = v[j];
+        }
+#pragma unroll
+        for (int o = 16; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+        float s = 0.0f;
+        if (mx != -INFINITY) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) s += __expf(v[j] - mx);
+        }
+#pragma unroll
+        for (int o = 16; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+        if ((lane & 31) == 0) red[wn * GBM + rl] = f32x2{mx, s};
+      }
+    }
+    __syncthreads();
+    const int row = m0 + tid;
+    if (row < M) {
+      const f32x2 a = red[tid], b = red[GBM + tid];
+      const float m = fmaxf(a.x, b.x);
+      const float s = (a.y > 0.0f ? a.y * __expf(a.x - m) : 0.0f) +
+                      (b.y > 0.0f ? b.y * __expf(b.x - m) : 0.0f);
+      part[(int64_t)tn * ld_part + row] = f32x2{m, s};
+    }
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ T to_store(float v);
+template <>
+__device__ __forceinline__ __bf16 to_store<__bf16>(float v) {
+  return __builtin_bit_cast(__bf16, f32_to_bf16_bits(v));
+}
+template <>
+__device__ __forceinline__ float to_store<float>(float v) {
+  return v;
+}
+
+// Backward recompute: G = gs_n * (1[v == y_n] - exp(z - lse_n)), rounded to T,
+// written both as G[row][col] and transposed as Gt[col][row].  Rows >= M and
+// columns >= N are written as 0 (they pad the K extent of the next products).
+template <typename T>
+struct EpiLogitGrad {
+  const int32_t* y;
+  const float* lse;
+  const float* gs;       // dL/dlogp / temperature, per compacted row
+  T* G;
+  int64_t ldg;
+  T* Gt;
+  int64_t ldgt;
+  float scale;
+  int32_t col0;          // vocabulary index of this chunk's column 0
+
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                             int N, uint8_t* smem, int wm, int wn, int lane,
+                                             int tid) const {
+    int* sy = (int*)smem;
+    float* sl = (float*)(smem + 1024);
+    float* sg = (float*)(smem + 2048);
+    const bool live = m0 + tid < M;
+    sy[tid] = live ? y[m0 + tid] - col0 : -1;
+    sl[tid] = live ? lse[m0 + tid] : 0.0f;
+    sg[tid] = live ? gs[m0 + tid] : 0.0f;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int cl = acc_col(wn, j, lane);
+          const int c = n0 + cl;
+          T vals[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int r = r4 * 4 + q;
+            const int rl = acc_row(wm, i, r, lane);
+            float gval = 0.0f;
+            if (c < N) {
+              const float z = acc[i][j][r] * scale;
+              const float p = __expf(z - sl[rl]);
+              gval = sg[rl] * ((c == sy[rl] ? 1.0f : 0.0f) - p);
+            }
+            vals[q] = to_store<T>(gval);
+            G[(int64_t)(m0 + rl) * ldg + c] = vals[q];
+          }
+          // four consecutive rows of one column: one vector store into Gt
+          const int rl0 = acc_row(wm, i, r4 * 4, lane);
+          T* dst = Gt + (int64_t)c * ldgt + m0 + rl0;
+          if constexpr (sizeof(T) == 2) {
+            u32x2 packed;
+            packed.x = (uint32_t)__builtin_bit_cast(uint16_t, vals[0]) |
+                       ((uint32_t)__builtin_bit_cast(uint16_t, vals[1]) << 16);
+            packed.y = (uint32_t)__builtin_bit_cast(uint16_t, vals[2]) |
+                       ((uint32_t)__builtin_bit_cast(uint16_t, vals[3]) << 16);
+            *(u32x2*)dst = packed;
+          } else {
+            *(f32x4*)dst = f32x4{(float)vals[0], (float)vals[1], (float)vals[2], (float)vals[3]};
+          }
+        }
+      }
+    }
+  }
+};
+
+// Plain fp32 store (or accumulate) of the tile, rows optionally remapped.
+struct EpiStore {
+  float* out;
+  int64_t ldo;
+  const int32_t* row_map;   // nullable: output row of each tile row
+  int32_t accumulate;
+
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                             int N, uint8_t* smem, int wm, int wn, int lane,
+                                             int tid) const {
+    int* sr = (int*)smem;
+    if (row_map) {
+      sr[tid] = (m0 + tid < M) ? row_map[m0 + tid] : 0;
+      __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = acc_row(wm, i, r, lane);
+        if (m0 + rl >= M) continue;
+        const int64_t orow = row_map ? (int64_t)sr[rl] : (int64_t)(m0 + rl);
+        float* dst = out + orow * ldo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = n0 + acc_col(wn, j, lane);
+          if (c < N) dst[c] = accumulate ? dst[c] + acc[i][j][r] : acc[i][j][r];
+        }
+      }
+  }
+};
+
+}  // namespace agrl

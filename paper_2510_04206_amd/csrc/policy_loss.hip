@@ -1,0 +1,749 @@
+// Fused LM-head + token log-probability + clipped policy-gradient loss, forward
+// and backward, over a packed micro-batch (AgentRL App. B.1 token-level
+// factorisation; App. B.2 PPO/GRPO clipped surrogate; App. A DAPO decoupled
+// clip bounds and token-level normalisation).
+//
+// Forward:  compact the action tokens -> logits H_act W^T by 256 x 256 tiles on
+//           the matrix cores with a per-tile max / sum-exp epilogue (logits are
+//           never written) -> merge the vocabulary tiles into lse -> logp,
+//           ratio, clipped surrogate, fixed-order loss sum.
+// Backward: recompute the logit tiles, form G = dL/dz in bf16 (both layouts),
+//           then dW = G^T H and dH = G W on the matrix cores; the vocabulary is
+//           processed in chunks that bound the G buffers.
+#include <math.h>
+
+#include "../../include/agrl.h"
+#include "common.hpp"
+#include "gemm.hpp"
+
+namespace agrl {
+namespace {
+
+constexpr int kScanTile = 4096;          // tokens per block of the compaction scan
+constexpr int kScanThreads = 256;
+constexpr int kScanPer = kScanTile / kScanThreads;   // 16 tokens per thread
+constexpr int kRowPad = 256;             // compacted rows are padded to the GEMM tile
+constexpr int kMergeThreads = 256;
+
+__host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+
+// ------------------------------------------------------------------ compaction
+__global__ __launch_bounds__(kScanThreads) void scan_count_kernel(int64_t T,
+                                                                  const uint8_t* __restrict__ mask,
+                                                                  int32_t* blk_cnt) {
+  __shared__ int wsum[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + threadIdx.x * kScanPer;
+  int c = 0;
+  for (int i = 0; i < kScanPer; ++i) {
+    const int64_t t = base + i;
+    if (t < T) c += mask[t] != 0;
+  }
+  for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int w = 0; w < kScanThreads / 64; ++w) s += wsum[w];
+    blk_cnt[blockIdx.x] = s;
+  }
+}
+
+// Single block: exclusive offsets of the scan blocks, the action count, and
+// the max_act check (an overflow zeroes the count and flags the call).
+__global__ __launch_bounds__(1024) void scan_offsets_kernel(int32_t nblk,
+                                                            const int32_t* __restrict__ blk_cnt,
+                                                            int32_t* blk_off, int32_t* ctrl,
+                                                            int64_t max_act, int* err) {
+  __shared__ int wsum[16];
+  __shared__ int carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int base = 0; base < nblk; base += 1024) {
+    const int i = base + threadIdx.x;
+    const int v = i < nblk ? blk_cnt[i] : 0;
+    int incl = v;   // inclusive prefix within the wave
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(incl, o);
+      if (lane >= o) incl += u;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int before = carry;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    if (i < nblk) blk_off[i] = before + incl - v;
+    __syncthreads();
+    if (threadIdx.x == 1023) carry = before + incl;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int total = carry;
+    if ((int64_t)total > max_act) {
+      set_error(err, ERR_MAX_ACT);
+      ctrl[0] = 0;
+      ctrl[1] = 1;      // loss becomes NaN
+    } else {
+      ctrl[0] = total;
+      ctrl[1] = 0;
+    }
+    ctrl[2] = total;
+  }
+}
+
+struct ScatterArgs {
+  int64_t T;
+  int32_t V;
+  int32_t nblk;
+  const uint8_t* mask;
+  const int32_t* token_id;
+  const float* adv_tok;
+  const float* old_logp;
+  const float* lse_in;      // backward only
+  const float* logp_in;     // backward only
+  const int32_t* blk_off;
+  const int32_t* ctrl;
+  int64_t cap;              // rows allocated for compacted arrays
+  int32_t* idx;
+  int32_t* y_act;
+  float* adv_act;
+  float* old_act;
+  float* lse_act;           // backward only
+  float* gs_act;            // backward only: dL/dlogp / temperature
+  float* logp_out;          // forward only: zeroed on masked tokens
+  float* lse_out;
+  float eps_lo, eps_hi;
+  float grad_loss;
+  int64_t n_norm;
+  float inv_temp;
+  int* err;
+};
+
+__global__ __launch_bounds__(kScanThreads) void scan_scatter_kernel(ScatterArgs a) {
+  __shared__ int wsum[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanTile + threadIdx.x * kScanPer;
+  uint8_t m[kScanPer];
+  int c = 0;
+  for (int i = 0; i < kScanPer; ++i) {
+    const int64_t t = base + i;
+    m[i] = (t < a.T) ? (a.mask[t] != 0) : 0;
+    c += m[i];
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = c;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(incl, o);
+    if (lane >= o) incl += u;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int pos = a.blk_off[blockIdx.x] + incl - c;
+  for (int w = 0; w < wave; ++w) pos += wsum[w];
+  const bool ok = a.ctrl[1] == 0;
+  const int n_act = a.ctrl[2];
+  const float N = a.n_norm > 0 ? (float)a.n_norm : (float)n_act;
+  for (int i = 0; i < kScanPer; ++i) {
+    const int64_t t = base + i;
+    if (t >= a.T) break;
+    if (!m[i]) {
+      if (a.logp_out) {
+        a.logp_out[t] = 0.0f;
+        a.lse_out[t] = 0.0f;
+      }
+      continue;
+    }
+    const int y = a.token_id[t];
+    if (y < 0 || y >= a.V) set_error(a.err, ERR_TOKEN_ID);
+    if (ok && pos < a.cap) {
+      a.idx[pos] = (int32_t)t;
+      a.y_act[pos] = y;
+      const float adv = a.adv_tok[t];
+      const float old = a.old_logp[t];
+      a.adv_act[pos] = adv;
+      a.old_act[pos] = old;
+      if (a.gs_act) {
+        // dL/dlogp of -(1/N) min(rho A, clip(rho) A): the unclipped branch's
+        // derivative, or 0 where the clipped branch is the active minimum.
+        const float lp = a.logp_in[t];
+        const float rho = expf(lp - old);
+        const bool cut = (adv > 0.0f && rho > 1.0f + a.eps_hi) || (adv < 0.0f && rho < 1.0f - a.eps_lo);
+        const float g = cut ? 0.0f : -(a.grad_loss / N) * adv * rho;
+        a.lse_act[pos] = a.lse_in[t];
+        a.gs_act[pos] = g * a.inv_temp;
+      }
+    }
+    ++pos;
+  }
+}
+
+// H_act[n] = H[idx[n]] for n < n_act, zero rows up to the next multiple of 256.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint8_t* __restrict__ H,
+                                                          int64_t row_bytes,
+                                                          const int32_t* __restrict__ idx,
+                                                          const int32_t* ctrl, uint8_t* H_act) {
+  const int n_act = ctrl[0];
+  const int64_t rows = round_up(n_act, kRowPad);
+  const int64_t chunks = row_bytes / 16;
+  for (int64_t n = blockIdx.x; n < rows; n += gridDim.x) {
+    u32x4* dst = (u32x4*)(H_act + n * row_bytes);
+    if (n < n_act) {
+      const u32x4* src = (const u32x4*)(H + (int64_t)idx[n] * row_bytes);
+      for (int64_t c = threadIdx.x; c < chunks; c += blockDim.x) dst[c] = src[c];
+    } else {
+      for (int64_t c = threadIdx.x; c < chunks; c += blockDim.x) dst[c] = u32x4{0, 0, 0, 0};
+    }
+  }
+}
+
+// dst[c][r] = src[r][c]; rows in [n_rows, n_rows_pad) are written as 0.
+// n_rows comes from ctrl[0] (rounded up to 256 for the padded extent) when
+// rows_from_ctrl is set.  64 x 64 element tiles through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ src, int64_t ld_src,
+                                                        T* dst, int64_t ld_dst, int64_t n_rows,
+                                                        int64_t n_rows_pad, int64_t n_cols,
+                                                        const int32_t* ctrl) {
+  __shared__ T tile[64][65];
+  if (ctrl) {
+    n_rows = ctrl[0];
+    n_rows_pad = round_up(n_rows, kRowPad);
+  }
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  if (r0 >= n_rows_pad) return;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int k = 0; k < 16; ++k) {
+    const int rr = ty + 4 * k;
+    const int64_t r = r0 + rr, c = c0 + tx;
+    T v = T(0);
+    if (r < n_rows && c < n_cols) v = src[r * ld_src + c];
+    tile[rr][tx] = v;
+  }
+  __syncthreads();
+  for (int k = 0; k < 16; ++k) {
+    const int cc = ty + 4 * k;
+    const int64_t c = c0 + cc, r = r0 + tx;
+    if (c < n_cols && r < n_rows_pad) dst[c * ld_dst + r] = tile[tx][cc];
+  }
+}
+
+// ------------------------------------------------------------------ forward epilogue
+struct MergeArgs {
+  const int32_t* ctrl;
+  int32_t tiles_v;
+  const f32x2* part;
+  int64_t ld_part;
+  const float* zy;
+  const float* old_act;
+  const float* adv_act;
+  const int32_t* idx;
+  float eps_lo, eps_hi;
+  float* logp_out;
+  float* lse_out;
+  double* blk_sum;
+  long long* blk_clip;     // [2 * blocks]
+};
+
+// One thread per action token: lse from the vocabulary-tile partials, then
+// logp, rho and the clipped surrogate; fixed-order block partial sums.
+__global__ __launch_bounds__(kMergeThreads) void merge_loss_kernel(MergeArgs a) {
+  __shared__ double ssum[kMergeThreads];
+  __shared__ long long shi[kMergeThreads], slo[kMergeThreads];
+  const int n_act = a.ctrl[0];
+  const int n = blockIdx.x * kMergeThreads + threadIdx.x;
+  double s = 0.0;
+  long long hi = 0, lo = 0;
+  if (n < n_act) {
+    float m = -INFINITY;
+    for (int t = 0; t < a.tiles_v; ++t) m = fmaxf(m, a.part[(int64_t)t * a.ld_part + n].x);
+    float sum = 0.0f;
+    for (int t = 0; t < a.tiles_v; ++t) {
+      const f32x2 p = a.part[(int64_t)t * a.ld_part + n];
+      if (p.y > 0.0f) sum += p.y * expf(p.x - m);
+    }
+    const float lse = m + logf(sum);
+    const float logp = a.zy[n] - lse;
+    const float A = a.adv_act[n];
+    const float rho = expf(logp - a.old_act[n]);
+    const float rc = fminf(fmaxf(rho, 1.0f - a.eps_lo), 1.0f + a.eps_hi);
+    s = (double)fminf(rho * A, rc * A);
+    hi = (A > 0.0f && rho > 1.0f + a.eps_hi);
+    lo = (A < 0.0f && rho < 1.0f - a.eps_lo);
+    const int t = a.idx[n];
+    a.logp_out[t] = logp;
+    a.lse_out[t] = lse;
+  }
+  ssum[threadIdx.x] = s;
+  shi[threadIdx.x] = hi;
+  slo[threadIdx.x] = lo;
+  __syncthreads();
+  for (int w = kMergeThreads / 2; w >= 1; w >>= 1) {
+    if (threadIdx.x < w) {
+      ssum[threadIdx.x] += ssum[threadIdx.x + w];
+      shi[threadIdx.x] += shi[threadIdx.x + w];
+      slo[threadIdx.x] += slo[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    a.blk_sum[blockIdx.x] = ssum[0];
+    a.blk_clip[2 * blockIdx.x] = shi[0];
+    a.blk_clip[2 * blockIdx.x + 1] = slo[0];
+  }
+}
+
+__global__ __launch_bounds__(256) void finalize_loss_kernel(int32_t nblk, const double* blk_sum,
+                                                            const long long* blk_clip,
+                                                            const int32_t* ctrl, int64_t n_norm,
+                                                            float* loss, int64_t* n_clip) {
+  __shared__ double ssum[256];
+  __shared__ long long shi[256], slo[256];
+  double s = 0.0;
+  long long hi = 0, lo = 0;
+  for (int b = threadIdx.x; b < nblk; b += 256) {
+    s += blk_sum[b];
+    hi += blk_clip[2 * b];
+    lo += blk_clip[2 * b + 1];
+  }
+  ssum[threadIdx.x] = s;
+  shi[threadIdx.x] = hi;
+  slo[threadIdx.x] = lo;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (threadIdx.x < w) {
+      ssum[threadIdx.x] += ssum[threadIdx.x + w];
+      shi[threadIdx.x] += shi[threadIdx.x + w];
+      slo[threadIdx.x] += slo[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int n_act = ctrl[0];
+    const double N = n_norm > 0 ? (double)n_norm : (double)n_act;
+    float L = N > 0 ? (float)(-ssum[0] / N) : 0.0f;
+    if (ctrl[1]) L = NAN;
+    *loss = L;
+    if (n_clip) {
+      n_clip[0] = shi[0];
+      n_clip[1] = slo[0];
+    }
+  }
+}
+
+__global__ void zero_loss_kernel(float* loss, int64_t* n_clip) {
+  *loss = 0.0f;
+  if (n_clip) {
+    n_clip[0] = 0;
+    n_clip[1] = 0;
+  }
+}
+
+__global__ __launch_bounds__(256) void zero_masked_rows_kernel(int64_t T, int32_t d,
+                                                               const uint8_t* __restrict__ mask,
+                                                               float* dH) {
+  for (int64_t t = blockIdx.x; t < T; t += gridDim.x) {
+    if (mask[t]) continue;
+    f32x4* row = (f32x4*)(dH + t * d);
+    for (int c = threadIdx.x; c < d / 4; c += blockDim.x) row[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+__global__ __launch_bounds__(256) void zero_f32_kernel(float* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0.0f;
+}
+
+// ------------------------------------------------------------------ host side
+int fail(int code, const char* msg) {
+  set_last_error(msg);
+  return code;
+}
+
+struct Layout {
+  int64_t T, A_pad, V_pad, Vc;
+  int32_t d, V, esize, nblk, tiles_v, merge_blocks;
+  size_t ctrl, blk_cnt, blk_off, idx, y_act, adv_act, old_act, lse_act, gs_act, zy, blk_sum,
+      blk_clip, H_act, part, Ht, Wt, G, Gt, total;
+};
+
+constexpr int64_t kDefaultChunkBytes = (int64_t)32 << 30;
+
+bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
+                 const agrl_options& o, Layout* L) {
+  if (T < 0 || d <= 0 || V <= 0 || (dtype != AGRL_BF16 && dtype != AGRL_F32)) return false;
+  if (max_act <= 0 || max_act > T) max_act = T;
+  L->T = T;
+  L->d = d;
+  L->V = V;
+  L->esize = dtype == AGRL_BF16 ? 2 : 4;
+  L->A_pad = round_up(max_act > 0 ? max_act : 1, kRowPad);
+  L->V_pad = round_up(V, kRowPad);
+  L->nblk = (int32_t)((T + kScanTile - 1) / kScanTile);
+  if (L->nblk < 1) L->nblk = 1;
+  L->tiles_v = (int32_t)(L->V_pad / GBN);
+  L->merge_blocks = (int32_t)(L->A_pad / kMergeThreads);
+  const int64_t budget = o.g_chunk_bytes > 0 ? o.g_chunk_bytes : kDefaultChunkBytes;
+  int64_t vc = budget / (2 * L->A_pad * L->esize) / kRowPad * kRowPad;
+  if (vc < kRowPad) vc = kRowPad;
+  L->Vc = vc < L->V_pad ? vc : L->V_pad;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  const size_t A = (size_t)L->A_pad;
+  L->ctrl = take(256);
+  L->blk_cnt = take(sizeof(int32_t) * L->nblk);
+  L->blk_off = take(sizeof(int32_t) * L->nblk);
+  L->idx = take(4 * A);
+  L->y_act = take(4 * A);
+  L->adv_act = take(4 * A);
+  L->old_act = take(4 * A);
+  L->lse_act = take(4 * A);
+  L->gs_act = take(4 * A);
+  L->zy = take(4 * A);
+  L->blk_sum = take(sizeof(double) * L->merge_blocks);
+  L->blk_clip = take(2 * sizeof(long long) * L->merge_blocks);
+  L->H_act = take(A * d * L->esize);
+  // the forward's partials and the backward's buffers share one region
+  const size_t shared_at = off;
+  L->part = take((size_t)L->tiles_v * A * 8);
+  const size_t fwd_end = off;
+  off = shared_at;
+  L->Ht = take((size_t)d * A * L->esize);
+  L->Wt = take((size_t)d * L->V_pad * L->esize);
+  L->G = take(A * (size_t)L->Vc * L->esize);
+  L->Gt = take((size_t)L->Vc * A * L->esize);
+  if (fwd_end > off) off = fwd_end;
+  L->total = off;
+  return true;
+}
+
+struct Common {
+  int64_t T, max_act;
+  int32_t d, V, dtype;
+  float eps_lo, eps_hi, inv_temp;
+  agrl_options o;
+};
+
+int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
+             const void* H, const void* W, const int32_t* token_id, const uint8_t* mask,
+             const float* adv, const float* old, float eps_lo, float eps_hi, int64_t n_norm,
+             const agrl_options* opt, void* ws, size_t ws_bytes, Common* c) {
+  char buf[200];
+  auto bad = [&](int code, const char* what) {
+    snprintf(buf, sizeof buf, "%s: %s", fn, what);
+    return fail(code, buf);
+  };
+  if (dtype != AGRL_BF16 && dtype != AGRL_F32) return bad(AGRL_E_DTYPE, "dtype must be AGRL_BF16 or AGRL_F32");
+  if (T < 0) return bad(AGRL_E_SHAPE, "T < 0");
+  if (T > ((int64_t)1 << 31) - kScanTile) return bad(AGRL_E_SHAPE, "T too large");
+  if (d <= 0 || V <= 0) return bad(AGRL_E_SHAPE, "d and V must be positive");
+  if (d % 64 != 0) return bad(AGRL_E_UNSUPPORTED, "d must be a multiple of 64");
+  if (n_norm < 0) return bad(AGRL_E_SHAPE, "n_norm < 0");
+  if (!(eps_lo >= 0.0f && eps_lo < 1.0f) || !(eps_hi >= 0.0f) || !isfinite(eps_hi))
+    return bad(AGRL_E_FLAGS, "clip bounds must satisfy 0 <= low < 1 and 0 <= high < inf");
+  agrl_options o = {};
+  if (opt) o = *opt;
+  if (!(o.temperature >= 0.0f) || !isfinite(o.temperature))
+    return bad(AGRL_E_FLAGS, "temperature must be finite and >= 0");
+  if (o.dw_accumulate != 0 && o.dw_accumulate != 1) return bad(AGRL_E_FLAGS, "dw_accumulate must be 0 or 1");
+  if (o.g_chunk_bytes < 0) return bad(AGRL_E_FLAGS, "g_chunk_bytes < 0");
+  if (T > 0 && (!H || !token_id || !mask || !adv || !old)) return bad(AGRL_E_NULL, "input pointer is NULL");
+  if (!W) return bad(AGRL_E_NULL, "W is NULL");
+  if (max_act <= 0 || max_act > T) max_act = T;
+  // every tile row offset and the G buffers use 32-bit row indices
+  if (round_up(max_act > 0 ? max_act : 1, kRowPad) > ((int64_t)1 << 30)) return bad(AGRL_E_SHAPE, "max_act too large");
+  Layout L;
+  make_layout(T, max_act, d, V, dtype, o, &L);
+  if (T > 0 && (!ws || ws_bytes < L.total)) return bad(AGRL_E_WORKSPACE, "workspace missing or too small");
+  if ((((uintptr_t)H | (uintptr_t)W | (uintptr_t)ws) & 15) != 0)
+    return bad(AGRL_E_SHAPE, "H, W and workspace must be 16-byte aligned");
+  c->T = T;
+  c->max_act = max_act;
+  c->d = d;
+  c->V = V;
+  c->dtype = dtype;
+  c->eps_lo = eps_lo;
+  c->eps_hi = eps_hi;
+  c->inv_temp = o.temperature == 0.0f ? 1.0f : 1.0f / o.temperature;
+  c->o = o;
+  return AGRL_OK;
+}
+
+enum Phase { PH_FWD = 0, PH_RECOMPUTE = 1, PH_DW = 2, PH_DH = 3 };
+
+template <typename T, class Epi>
+void launch_gemm(const GemmShape& g, int max_tiles, const Epi& epi, const agrl_options& o,
+                 Phase ph, hipStream_t s) {
+  int grid = device_cu_count();
+  if (max_tiles < grid) grid = max_tiles < 1 ? 1 : max_tiles;
+  hipEvent_t* ev = (hipEvent_t*)o.phase_events;
+  if (ev) hipEventRecord(ev[2 * ph], s);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g, epi);
+  if (ev) hipEventRecord(ev[2 * ph + 1], s);
+}
+
+int compact(const Common& c, const Layout& L, uint8_t* ws, const uint8_t* mask,
+            const int32_t* token_id, const float* adv, const float* old, const float* lse_in,
+            const float* logp_in, float grad_loss, int64_t n_norm, float* logp_out,
+            float* lse_out, const void* H, int* err, hipStream_t s) {
+  int32_t* ctrl = (int32_t*)(ws + L.ctrl);
+  hipLaunchKernelGGL(scan_count_kernel, dim3(L.nblk), dim3(kScanThreads), 0, s, c.T, mask,
+                     (int32_t*)(ws + L.blk_cnt));
+  hipLaunchKernelGGL(scan_offsets_kernel, dim3(1), dim3(1024), 0, s, L.nblk,
+                     (const int32_t*)(ws + L.blk_cnt), (int32_t*)(ws + L.blk_off), ctrl,
+                     c.max_act, err);
+  ScatterArgs a;
+  a.T = c.T;
+  a.V = c.V;
+  a.nblk = L.nblk;
+  a.mask = mask;
+  a.token_id = token_id;
+  a.adv_tok = adv;
+  a.old_logp = old;
+  a.lse_in = lse_in;
+  a.logp_in = logp_in;
+  a.blk_off = (const int32_t*)(ws + L.blk_off);
+  a.ctrl = ctrl;
+  a.cap = L.A_pad;
+  a.idx = (int32_t*)(ws + L.idx);
+  a.y_act = (int32_t*)(ws + L.y_act);
+  a.adv_act = (float*)(ws + L.adv_act);
+  a.old_act = (float*)(ws + L.old_act);
+  a.lse_act = lse_in ? (float*)(ws + L.lse_act) : nullptr;
+  a.gs_act = lse_in ? (float*)(ws + L.gs_act) : nullptr;
+  a.logp_out = logp_out;
+  a.lse_out = lse_out;
+  a.eps_lo = c.eps_lo;
+  a.eps_hi = c.eps_hi;
+  a.grad_loss = grad_loss;
+  a.n_norm = n_norm;
+  a.inv_temp = c.inv_temp;
+  a.err = err;
+  hipLaunchKernelGGL(scan_scatter_kernel, dim3(L.nblk), dim3(kScanThreads), 0, s, a);
+  const int64_t rows = L.A_pad;
+  const int grid = (int)(rows < 4096 ? rows : 4096);
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(grid), dim3(256), 0, s, (const uint8_t*)H,
+                     (int64_t)c.d * L.esize, (const int32_t*)(ws + L.idx), (const int32_t*)ctrl,
+                     ws + L.H_act);
+  return AGRL_OK;
+}
+
+template <typename T>
+void fwd_gemm(const Common& c, const Layout& L, uint8_t* ws, const void* W, hipStream_t s) {
+  GemmShape g = {};
+  g.A = ws + L.H_act;
+  g.lda = c.d;
+  g.B = W;
+  g.ldb = c.d;
+  g.m_dev = (const int32_t*)(ws + L.ctrl);
+  g.N = c.V;
+  g.K = c.d;
+  g.group_m = 8;
+  EpiLsePartial e;
+  e.y = (const int32_t*)(ws + L.y_act);
+  e.part = (f32x2*)(ws + L.part);
+  e.ld_part = L.A_pad;
+  e.zy = (float*)(ws + L.zy);
+  e.scale = c.inv_temp;
+  const int max_tiles = (int)(L.A_pad / GBM) * L.tiles_v;
+  launch_gemm<T>(g, max_tiles, e, c.o, PH_FWD, s);
+}
+
+template <typename T>
+struct Storage {
+  typedef uint16_t type;   // bf16 moved as raw bits
+};
+template <>
+struct Storage<float> {
+  typedef float type;
+};
+
+template <typename T>
+void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, float* dH, float* dW,
+               hipStream_t s) {
+  typedef typename Storage<T>::type S;
+  const int32_t* ctrl = (const int32_t*)(ws + L.ctrl);
+  T* Ht = (T*)(ws + L.Ht);
+  T* Wt = (T*)(ws + L.Wt);
+  T* G = (T*)(ws + L.G);
+  T* Gt = (T*)(ws + L.Gt);
+  // H_act^T [d][A_pad] (zero beyond the action rows) and W^T [d][V_pad] (zero beyond V)
+  hipLaunchKernelGGL((transpose_kernel<S>), dim3((unsigned)(L.A_pad / 64), (unsigned)cdiv(c.d, 64)),
+                     dim3(256), 0, s, (const S*)(ws + L.H_act), (int64_t)c.d, (S*)Ht, L.A_pad,
+                     (int64_t)0, (int64_t)0, (int64_t)c.d, ctrl);
+  hipLaunchKernelGGL((transpose_kernel<S>), dim3((unsigned)(L.V_pad / 64), (unsigned)cdiv(c.d, 64)),
+                     dim3(256), 0, s, (const S*)W, (int64_t)c.d, (S*)Wt, L.V_pad, (int64_t)c.V,
+                     L.V_pad, (int64_t)c.d, (const int32_t*)nullptr);
+  const int row_tiles = (int)(L.A_pad / GBM);
+  const int d_tiles = cdiv(c.d, GBN);
+  for (int64_t v0 = 0; v0 < c.V; v0 += L.Vc) {
+    const int32_t nv = (int32_t)((c.V - v0) < L.Vc ? (c.V - v0) : L.Vc);
+    const int nv_tiles = cdiv(nv, GBN);
+    {  // logits of the chunk -> G, Gt
+      GemmShape g = {};
+      g.A = ws + L.H_act;
+      g.lda = c.d;
+      g.B = (const uint8_t*)W + v0 * c.d * (int64_t)sizeof(T);
+      g.ldb = c.d;
+      g.m_dev = ctrl;
+      g.N = nv;
+      g.K = c.d;
+      g.group_m = 8;
+      EpiLogitGrad<T> e;
+      e.y = (const int32_t*)(ws + L.y_act);
+      e.lse = (const float*)(ws + L.lse_act);
+      e.gs = (const float*)(ws + L.gs_act);
+      e.G = G;
+      e.ldg = L.Vc;
+      e.Gt = Gt;
+      e.ldgt = L.A_pad;
+      e.scale = c.inv_temp;
+      e.col0 = (int32_t)v0;
+      launch_gemm<T>(g, row_tiles * nv_tiles, e, c.o, PH_RECOMPUTE, s);
+    }
+    {  // dW[v0 : v0 + nv] = Gt H_act  (K = action tokens)
+      GemmShape g = {};
+      g.A = Gt;
+      g.lda = L.A_pad;
+      g.B = Ht;
+      g.ldb = L.A_pad;
+      g.M = nv;
+      g.N = c.d;
+      g.k_dev = ctrl;
+      g.group_m = 8;
+      EpiStore e;
+      e.out = dW + v0 * c.d;
+      e.ldo = c.d;
+      e.row_map = nullptr;
+      e.accumulate = c.o.dw_accumulate;
+      launch_gemm<T>(g, nv_tiles * d_tiles, e, c.o, PH_DW, s);
+    }
+    {  // dH[idx] (+)= G W[v0 : v0 + nv]  (K = vocabulary columns of the chunk)
+      GemmShape g = {};
+      g.A = G;
+      g.lda = L.Vc;
+      g.B = Wt + v0;
+      g.ldb = L.V_pad;
+      g.m_dev = ctrl;
+      g.N = c.d;
+      g.K = (int32_t)round_up(nv, KStage<T>::BK);
+      g.group_m = 8;
+      EpiStore e;
+      e.out = dH;
+      e.ldo = c.d;
+      e.row_map = (const int32_t*)(ws + L.idx);
+      e.accumulate = v0 > 0;
+      launch_gemm<T>(g, row_tiles * d_tiles, e, c.o, PH_DH, s);
+    }
+  }
+}
+
+}  // namespace
+}  // namespace agrl
+
+extern "C" size_t agrl_policy_loss_workspace_size(int64_t T, int64_t max_act, int32_t d,
+                                                  int32_t V, int32_t dtype,
+                                                  const agrl_options* opt) {
+  agrl_options o = {};
+  if (opt) o = *opt;
+  agrl::Layout L;
+  if (T <= 0 || o.g_chunk_bytes < 0 || !agrl::make_layout(T, max_act, d, V, dtype, o, &L)) return 0;
+  return L.total;
+}
+
+extern "C" int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32_t V,
+                                    int32_t dtype, const void* H, const void* W,
+                                    const int32_t* token_id, const uint8_t* action_mask,
+                                    const float* adv_tok, const float* old_logp,
+                                    float clip_eps_low, float clip_eps_high, int64_t n_norm,
+                                    const agrl_options* opt, void* workspace, size_t ws_bytes,
+                                    float* loss, float* logp, float* lse, int64_t* n_clip,
+                                    void* stream) {
+  using namespace agrl;
+  Common c;
+  int rc = validate("agrl_policy_loss_fwd", T, max_act, d, V, dtype, H, W, token_id, action_mask,
+                    adv_tok, old_logp, clip_eps_low, clip_eps_high, n_norm, opt, workspace,
+                    ws_bytes, &c);
+  if (rc) return rc;
+  if (!loss || (T > 0 && (!logp || !lse))) return fail(AGRL_E_NULL, "agrl_policy_loss_fwd: output pointer is NULL");
+  hipStream_t s = (hipStream_t)stream;
+  int* err = device_error_ptr();
+  if (!err) return hip_status(hipErrorInvalidSymbol);
+  if (T == 0) {
+    hipLaunchKernelGGL(zero_loss_kernel, dim3(1), dim3(1), 0, s, loss, n_clip);
+    return hip_status(hipGetLastError());
+  }
+  Layout L;
+  make_layout(T, c.max_act, d, V, dtype, c.o, &L);
+  uint8_t* ws = (uint8_t*)workspace;
+  compact(c, L, ws, action_mask, token_id, adv_tok, old_logp, nullptr, nullptr, 0.0f, n_norm,
+          logp, lse, H, err, s);
+  if (dtype == AGRL_BF16)
+    fwd_gemm<__bf16>(c, L, ws, W, s);
+  else
+    fwd_gemm<float>(c, L, ws, W, s);
+  MergeArgs m;
+  m.ctrl = (const int32_t*)(ws + L.ctrl);
+  m.tiles_v = L.tiles_v;
+  m.part = (const f32x2*)(ws + L.part);
+  m.ld_part = L.A_pad;
+  m.zy = (const float*)(ws + L.zy);
+  m.old_act = (const float*)(ws + L.old_act);
+  m.adv_act = (const float*)(ws + L.adv_act);
+  m.idx = (const int32_t*)(ws + L.idx);
+  m.eps_lo = c.eps_lo;
+  m.eps_hi = c.eps_hi;
+  m.logp_out = logp;
+  m.lse_out = lse;
+  m.blk_sum = (double*)(ws + L.blk_sum);
+  m.blk_clip = (long long*)(ws + L.blk_clip);
+  hipLaunchKernelGGL(merge_loss_kernel, dim3(L.merge_blocks), dim3(kMergeThreads), 0, s, m);
+  hipLaunchKernelGGL(finalize_loss_kernel, dim3(1), dim3(256), 0, s, L.merge_blocks,
+                     (const double*)(ws + L.blk_sum), (const long long*)(ws + L.blk_clip),
+                     (const int32_t*)(ws + L.ctrl), n_norm, loss, n_clip);
+  return hip_status(hipGetLastError());
+}
+
+extern "C" int agrl_policy_loss_bwd(int64_t T, int64_t max_act, int32_t d, int32_t V,
+                                    int32_t dtype, const void* H, const void* W,
+                                    const int32_t* token_id, const uint8_t* action_mask,
+                                    const float* adv_tok, const float* old_logp,
+                                    float clip_eps_low, float clip_eps_high, int64_t n_norm,
+                                    const agrl_options* opt, const float* lse, const float* logp,
+                                    float grad_loss, void* workspace, size_t ws_bytes, float* dH,
+                                    float* dW, void* stream) {
+  using namespace agrl;
+  Common c;
+  int rc = validate("agrl_policy_loss_bwd", T, max_act, d, V, dtype, H, W, token_id, action_mask,
+                    adv_tok, old_logp, clip_eps_low, clip_eps_high, n_norm, opt, workspace,
+                    ws_bytes, &c);
+  if (rc) return rc;
+  if (!dW || (T > 0 && (!dH || !lse || !logp)))
+    return fail(AGRL_E_NULL, "agrl_policy_loss_bwd: lse/logp/dH/dW pointer is NULL");
+  if (!isfinite(grad_loss)) return fail(AGRL_E_FLAGS, "agrl_policy_loss_bwd: grad_loss must be finite");
+  hipStream_t s = (hipStream_t)stream;
+  int* err = device_error_ptr();
+  if (!err) return hip_status(hipErrorInvalidSymbol);
+  if (T == 0) {
+    if (!c.o.dw_accumulate) {
+      const int64_t n = (int64_t)V * d;
+      hipLaunchKernelGGL(zero_f32_kernel, dim3((unsigned)(n / 256 < 4096 ? n / 256 + 1 : 4096)),
+                         dim3(256), 0, s, dW, n);
+    }
+    return hip_status(hipGetLastError());
+  }
+  Layout L;
+  make_layout(T, c.max_act, d, V, dtype, c.o, &L);
+  uint8_t* ws = (uint8_t*)workspace;
+  compact(c, L, ws, action_mask, token_id, adv_tok, old_logp, lse, logp, grad_loss, n_norm,
+          nullptr, nullptr, H, err, s);
+  hipLaunchKernelGGL(zero_masked_rows_kernel, dim3((unsigned)(T < 8192 ? T : 8192)), dim3(256), 0,
+                     s, T, d, action_mask, dH);
+  if (dtype == AGRL_BF16)
+    bwd_gemms<__bf16>(c, L, ws, W, dH, dW, s);
+  else
+    bwd_gemms<float>(c, L, ws, W, dH, dW, s);
+  return hip_status(hipGetLastError());
+}

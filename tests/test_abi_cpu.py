@@ -1,0 +1,141 @@
+"""The C ABI library on the CPU: it loads, exports every declared symbol, and
+rejects bad arguments synchronously (before any HIP call, so no GPU is needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "agrl.h")
+
+E_NULL, E_SHAPE, E_DTYPE, E_FLAGS, E_WS, E_HIP, E_UNSUP = -1, -2, -3, -4, -5, -6, -7
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(agrl_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2510_04206_amd import _binding
+    return _binding.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared()
+    assert {"agrl_task_adv_norm", "agrl_policy_loss_fwd", "agrl_policy_loss_bwd",
+            "agrl_policy_loss_workspace_size"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+    from paper_2510_04206_amd import _binding
+    assert set(_binding.exported_symbols()) == set(names)
+
+
+def test_status_strings(L):
+    for code in (0, E_NULL, E_SHAPE, E_DTYPE, E_FLAGS, E_WS, E_HIP, E_UNSUP):
+        assert L.agrl_status_string(code)
+    assert L.agrl_status_string(12345) == b"unknown status"
+
+
+def _fwd(L, **kw):
+    a = dict(T=100, max_act=0, d=64, V=50, dt=0, H=1 << 12, W=1 << 12, ids=1 << 12, m=1 << 12,
+             adv=1 << 12, old=1 << 12, lo=0.2, hi=0.2, n_norm=0, opt=None, ws=None, wsb=0,
+             loss=1 << 12, logp=1 << 12, lse=1 << 12, ncl=None)
+    a.update(kw)
+    return L.agrl_policy_loss_fwd(a["T"], a["max_act"], a["d"], a["V"], a["dt"], a["H"], a["W"],
+                                  a["ids"], a["m"], a["adv"], a["old"], a["lo"], a["hi"],
+                                  a["n_norm"], a["opt"], a["ws"], a["wsb"], a["loss"], a["logp"],
+                                  a["lse"], a["ncl"], None)
+
+
+def test_forward_argument_errors(L):
+    from paper_2510_04206_amd._binding import agrl_options
+    assert _fwd(L, dt=7) == E_DTYPE
+    assert _fwd(L, T=-1) == E_SHAPE
+    assert _fwd(L, d=0) == E_SHAPE
+    assert _fwd(L, V=0) == E_SHAPE
+    assert _fwd(L, d=100) == E_UNSUP
+    assert _fwd(L, lo=1.0) == E_FLAGS
+    assert _fwd(L, lo=-0.1) == E_FLAGS
+    assert _fwd(L, hi=float("inf")) == E_FLAGS
+    assert _fwd(L, hi=float("nan")) == E_FLAGS
+    assert _fwd(L, n_norm=-3) == E_SHAPE
+    assert _fwd(L, H=None) == E_NULL
+    assert _fwd(L, W=None) == E_NULL
+    assert _fwd(L, ws=None) == E_WS
+    assert b"workspace" in L.agrl_last_error()
+    o = agrl_options(temperature=-1.0)
+    assert _fwd(L, opt=ctypes.byref(o)) == E_FLAGS
+    o = agrl_options(dw_accumulate=2)
+    assert _fwd(L, opt=ctypes.byref(o)) == E_FLAGS
+    # a workspace that is one byte short
+    need = L.agrl_policy_loss_workspace_size(100, 0, 64, 50, 0, None)
+    assert _fwd(L, ws=1 << 12, wsb=need - 1) == E_WS
+
+
+def test_backward_argument_errors(L):
+    def bwd(**kw):
+        a = dict(lse=1 << 12, logp=1 << 12, g=1.0, dH=1 << 12, dW=1 << 12, d=64)
+        a.update(kw)
+        return L.agrl_policy_loss_bwd(10, 0, a["d"], 50, 0, 1 << 12, 1 << 12, 1 << 12, 1 << 12,
+                                      1 << 12, 1 << 12, 0.2, 0.2, 0, None, a["lse"], a["logp"],
+                                      a["g"], None, 0, a["dH"], a["dW"], None)
+    assert bwd(d=65) == E_UNSUP
+    assert bwd() == E_WS
+    need = L.agrl_policy_loss_workspace_size(10, 0, 64, 50, 0, None)
+    assert L.agrl_policy_loss_bwd(10, 0, 64, 50, 0, 1 << 12, 1 << 12, 1 << 12, 1 << 12, 1 << 12,
+                                  1 << 12, 0.2, 0.2, 0, None, None, 1 << 12, 1.0, 1 << 12, need,
+                                  1 << 12, 1 << 12, None) == E_NULL
+    assert L.agrl_policy_loss_bwd(10, 0, 64, 50, 0, 1 << 12, 1 << 12, 1 << 12, 1 << 12, 1 << 12,
+                                  1 << 12, 0.2, 0.2, 0, None, 1 << 12, 1 << 12, float("inf"),
+                                  1 << 12, need, 1 << 12, 1 << 12, None) == E_FLAGS
+
+
+def test_adv_norm_argument_errors(L):
+    p = 1 << 12
+    f = L.agrl_task_adv_norm
+    assert f(-1, 1, 1, 0, p, p, p, None, p, None, p, p, p, p, p, None, None) == E_SHAPE
+    assert f(10, 1, 1, 0, None, p, p, None, p, None, p, p, p, p, p, None, None) == E_NULL
+    assert f(10, 1, 1, 0, p, p, p, p, p, None, p, p, p, p, p, None, None) == E_SHAPE  # n_group 0
+    assert f(10, 1, 1, 0, p, p, None, None, p, None, p, p, p, p, p, None, None) == E_NULL
+    assert f(10, 1, 1, 0, p, p, p, None, p, None, p, None, p, p, p, None, None) == E_NULL
+    from paper_2510_04206_amd._binding import agrl_options
+    o = agrl_options(std_ddof=2)
+    assert f(10, 1, 1, 0, p, p, p, None, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
+    o = agrl_options(std_eps=-1.0)
+    assert f(10, 1, 1, 0, p, p, p, None, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
+
+
+def test_workspace_size(L):
+    f = L.agrl_policy_loss_workspace_size
+    assert f(0, 0, 64, 50, 0, None) == 0
+    assert f(10, 0, 64, 50, 9, None) == 0
+    small = f(65536, 1000, 5120, 152064, 0, None)
+    big = f(65536, 20000, 5120, 152064, 0, None)
+    assert 0 < small < big
+    assert f(65536, 0, 5120, 152064, 0, None) >= big            # max_act <= 0 means T
+    assert f(4096, 0, 256, 4096, 1, None) > f(4096, 0, 256, 4096, 0, None)   # fp32 is larger
+    # the G budget bounds the chunked buffers
+    from paper_2510_04206_amd._binding import agrl_options
+    o = agrl_options(g_chunk_bytes=1 << 26)
+    assert f(65536, 20000, 5120, 152064, 0, ctypes.byref(o)) < big
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    from paper_2510_04206_amd import _binding
+    monkeypatch.setattr(_binding, "_lib", None)
+    monkeypatch.setattr(_binding, "LIB_PATH", "/nonexistent/libagrl.so")
+    with pytest.raises(ImportError):
+        _binding.lib()
+
+
+def test_product_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2510_04206_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                src = open(os.path.join(dirpath, fn)).read()
+                assert "oracle" not in src.lower(), fn

@@ -1,0 +1,96 @@
+"""GPU parity of agrl_task_adv_norm against the oracle: bit-exact (MI355X)."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import gen
+
+from helpers import adv_inputs, log
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("act_count", "task_count", "task_mean", "task_std", "adv_traj", "adv_tok")
+
+
+def _gpu(traj_id, mask, traj_task, traj_group, reward, n_task, n_group, ddof=0):
+    import paper_2510_04206_amd as P
+    dev = "cuda"
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    out = P.task_adv_norm(t(traj_id), t(mask), t(traj_task),
+                          None if traj_group is None else t(traj_group), t(reward), n_task,
+                          n_group, opt={"std_ddof": ddof})
+    assert P.agrl_get_device_error() == 0
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def _assert_bitwise(g, r):
+    for k in KEYS:
+        a, b = np.asarray(g[k]), np.asarray(r[k])
+        if a.dtype == np.float32:
+            np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32), err_msg=k)
+        else:
+            np.testing.assert_array_equal(a, b, err_msg=k)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("groups", [True, False])
+@pytest.mark.parametrize("ddof", [0, 1])
+def test_adv_norm_bit_exact(k, groups, ddof):
+    w = gen.config(k, tensors=False)
+    log(f"adv_norm workload {k} groups={groups} ddof={ddof} T_g={w.T_g}")
+    tg = w.traj_group if groups else None
+    r = oracle.task_adv_norm(w.g_traj_id, w.g_mask, w.traj_task, tg, w.reward, w.n_task,
+                             w.n_group, ddof=ddof)
+    g = _gpu(w.g_traj_id, w.g_mask, w.traj_task, tg, w.reward, w.n_task, w.n_group, ddof)
+    _assert_bitwise(g, r)
+
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "adv_norm_cases.json")
+
+
+@pytest.mark.parametrize("case", json.load(open(GOLDEN))["cases"], ids=lambda c: c["name"])
+def test_adv_norm_golden_cases(case):
+    log(f"adv_norm golden {case['name']}")
+    tg = None if case["traj_group"] is None else np.array(case["traj_group"], np.int32)
+    args = (np.array(case["traj_id"], np.int32), np.array(case["mask"], np.uint8),
+            np.array(case["traj_task"], np.int32), tg, np.array(case["reward"], np.float32),
+            case["n_task"], case["n_group"])
+    r = oracle.task_adv_norm(*args, ddof=case["ddof"])
+    g = _gpu(*args, ddof=case["ddof"])
+    _assert_bitwise(g, r)
+
+
+def test_adv_norm_edge_cases():
+    """Empty trajectories, a task with no action tokens, padding tokens, many tasks."""
+    rng = np.random.default_rng(3)
+    n_traj, n_task, n_group = 300, 7, 75
+    traj_task = rng.integers(0, n_task - 1, n_traj).astype(np.int32)   # task n_task-1 empty
+    traj_group = (np.arange(n_traj) // 4).astype(np.int32)
+    reward = rng.standard_normal(n_traj).astype(np.float32)
+    T_g = 20011
+    traj_id = rng.integers(-1, n_traj, T_g).astype(np.int32)
+    traj_id[traj_id == 17] = 18                                      # trajectory 17 has no tokens
+    mask = (rng.random(T_g) < 0.4).astype(np.uint8)
+    log("adv_norm edge cases")
+    for tg in (traj_group, None):
+        args = (traj_id, mask, traj_task, tg, reward, n_task, n_group)
+        _assert_bitwise(_gpu(*args), oracle.task_adv_norm(*args))
+
+
+def test_adv_norm_out_of_range_ids_flagged():
+    import paper_2510_04206_amd as P
+    log("adv_norm out-of-range ids")
+    traj_id = np.array([0, 1, 5], np.int32)
+    mask = np.ones(3, np.uint8)
+    t = lambda a: torch.from_numpy(a).cuda()
+    P.task_adv_norm(t(traj_id), t(mask), t(np.array([0, 0], np.int32)), None,
+                    t(np.array([1.0, 0.0], np.float32)), 1)
+    assert P.agrl_get_device_error() & 2
+    P.task_adv_norm(t(traj_id[:2]), t(mask[:2]), t(np.array([0, 3], np.int32)), None,
+                    t(np.array([1.0, 0.0], np.float32)), 1)
+    assert P.agrl_get_device_error() & 4
+    assert P.agrl_get_device_error() == 0
