@@ -4,10 +4,10 @@
 // Block tile 256 x 256, 4 waves in a 2 x 2 arrangement, each wave owning a
 // 128 x 128 sub-tile as 4 x 4 blocks of 32 x 32 MFMA accumulators
 // (v_mfma_f32_32x32x16_bf16 for bf16, v_mfma_f32_32x32x2_f32 for fp32).
-// Each K stage moves 128 bytes of every tile row (64 bf16 or 32 fp32) through
-// LDS, double-buffered with one barrier per stage; 16-byte chunks are stored
-// at chunk ^ (row & 7) so that both the row-wise writes and the 32-row
-// fragment reads are free of bank conflicts.
+// Each K stage moves 128 bytes of every tile row (64 bf16 or 32 fp32) from
+// global memory straight into LDS (no register staging), double-buffered with
+// one barrier per stage; 16-byte chunks are stored at chunk ^ (row & 7) so the
+// 32-row fragment reads are free of bank conflicts.
 //
 // The grid is persistent (about one workgroup per compute unit, since a block
 // holds 128 KiB of LDS).  The row count M and the K extent may be read from
@@ -78,30 +78,29 @@ __device__ __forceinline__ void map_tile(int t, int grid, int total, int tiles_m
   tn = rem / gsz;
 }
 
-// One K stage of global loads: 8 16-byte chunks of A and of B per thread.
-__device__ __forceinline__ void load_stage(u32x4 (&ra)[8], u32x4 (&rb)[8], const uint8_t* A,
-                                           int64_t lda_b, int m0, int M, const uint8_t* B,
-                                           int64_t ldb_b, int n0, int N, int64_t k0_b, int tid) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int q = tid + GEMM_THREADS * i;
-    const int r = q >> 3, c = q & 7;
-    const int64_t ra_row = min(m0 + r, M - 1);
-    const int64_t rb_row = min(n0 + r, N - 1);
-    ra[i] = *(const u32x4*)(A + ra_row * lda_b + k0_b + c * 16);
-    rb[i] = *(const u32x4*)(B + rb_row * ldb_b + k0_b + c * 16);
-  }
-}
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
 
-__device__ __forceinline__ void store_stage(uint8_t* st, const u32x4 (&ra)[8],
-                                            const u32x4 (&rb)[8], int tid) {
+// One K stage as direct global -> LDS copies (global_load_lds_dwordx4): each
+// instruction moves 8 tile rows (1 KiB) and writes LDS contiguously, lane i at
+// byte 16 * i.  Lane i therefore fetches logical chunk (i & 7) ^ (row & 7) of
+// row i / 8, which lands it at the swizzled position.  Wave w copies rows
+// [64 w, 64 w + 64) of both the A and the B tile.  Rows past M or N are clamped
+// to the last valid row (their products are discarded by the epilogue).
+__device__ __forceinline__ void dma_stage(uint8_t* st, const uint8_t* A, int64_t lda_b, int m0,
+                                          int M, const uint8_t* B, int64_t ldb_b, int n0, int N,
+                                          int64_t k0_b, int wave, int lane) {
+  const int rl = lane >> 3;
+  const int c = (lane & 7) ^ rl;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int q = tid + GEMM_THREADS * i;
-    const int r = q >> 3, c = q & 7;
-    const int off = r * LDS_ROW + ((c ^ (r & 7)) << 4);
-    *(u32x4*)(st + off) = ra[i];
-    *(u32x4*)(st + GBM * LDS_ROW + off) = rb[i];
+  for (int b = 0; b < 8; ++b) {
+    const int r0 = wave * 64 + b * 8;
+    const int64_t ra = min(m0 + r0 + rl, M - 1);
+    const int64_t rb = min(n0 + r0 + rl, N - 1);
+    __builtin_amdgcn_global_load_lds((glb_void_t*)(A + ra * lda_b + k0_b + c * 16),
+                                     (lds_void_t*)(st + r0 * LDS_ROW), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((glb_void_t*)(B + rb * ldb_b + k0_b + c * 16),
+                                     (lds_void_t*)(st + GBM * LDS_ROW + r0 * LDS_ROW), 16, 0, 0);
   }
 }
 
@@ -109,25 +108,43 @@ template <typename T>
 __device__ __forceinline__ void compute_stage(const uint8_t* st, f32x16 (&acc)[4][4], int wm,
                                               int wn, int lane);
 
+// bf16: four 16-deep k slices per stage.  Each slice runs half of its 16
+// MFMAs, then issues the LDS reads of the next slice, then the other half, so
+// the wait before a slice only covers reads issued about 256 cycles earlier.
+// (sched_barrier pins that order; the scheduler would otherwise sink every
+// read next to its first use.)
 template <>
 __device__ __forceinline__ void compute_stage<__bf16>(const uint8_t* st, f32x16 (&acc)[4][4],
                                                       int wm, int wn, int lane) {
   const int sw = lane & 7;
   const uint8_t* As = st + (wm * 128 + (lane & 31)) * LDS_ROW;
   const uint8_t* Bs = st + GBM * LDS_ROW + (wn * 128 + (lane & 31)) * LDS_ROW;
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
+  bf16x8 a[2][4], b[2][4];
+  auto load = [&](int kk, bf16x8(&fa)[4], bf16x8(&fb)[4]) {
     const int chunk = ((kk * 2 + (lane >> 5)) ^ sw) << 4;
-    bf16x8 a[4], b[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(As + i * 32 * LDS_ROW + chunk);
+    for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8*)(As + i * 32 * LDS_ROW + chunk);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(Bs + j * 32 * LDS_ROW + chunk);
+    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)(Bs + j * 32 * LDS_ROW + chunk);
+  };
+  auto mfma_rows = [&](int kk, int i0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = i0; i < i0 + 2; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk & 1][i], b[kk & 1][j], acc[i][j],
+                                                            0, 0, 0);
+  };
+  load(0, a[0], b[0]);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    mfma_rows(kk, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kk < 3) load(kk + 1, a[(kk + 1) & 1], b[(kk + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_rows(kk, 2);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -195,18 +212,16 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     if (nk > 0) {
-      u32x4 ra[8], rb[8];
-      load_stage(ra, rb, A, lda_b, m0, M, B, ldb_b, n0, g.N, 0, tid);
-      store_stage(smem, ra, rb, tid);
+      dma_stage(smem, A, lda_b, m0, M, B, ldb_b, n0, g.N, 0, wave, lane);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       for (int kt = 0; kt < nk; ++kt) {
         const uint8_t* cur = smem + (kt & 1) * STAGE_BYTES;
-        const bool more = kt + 1 < nk;
-        if (more)
-          load_stage(ra, rb, A, lda_b, m0, M, B, ldb_b, n0, g.N,
-                     (int64_t)(kt + 1) * BK * (int64_t)sizeof(T), tid);
+        if (kt + 1 < nk)
+          dma_stage(smem + ((kt + 1) & 1) * STAGE_BYTES, A, lda_b, m0, M, B, ldb_b, n0, g.N,
+                    (int64_t)(kt + 1) * BK * (int64_t)sizeof(T), wave, lane);
         compute_stage<T>(cur, acc, wm, wn, lane);
-        if (more) store_stage(smem + ((kt + 1) & 1) * STAGE_BYTES, ra, rb, tid);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
       }
     }

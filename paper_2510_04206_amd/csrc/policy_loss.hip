@@ -23,7 +23,7 @@ constexpr int kScanTile = 4096;          // tokens per block of the compaction s
 constexpr int kScanThreads = 256;
 constexpr int kScanPer = kScanTile / kScanThreads;   // 16 tokens per thread
 constexpr int kRowPad = 256;             // compacted rows are padded to the GEMM tile
-constexpr int kMergeThreads = 256;
+constexpr int kMergeRows = 64;         // action tokens per merge block
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
@@ -242,51 +242,56 @@ struct MergeArgs {
   long long* blk_clip;     // [2 * blocks]
 };
 
-// One thread per action token: lse from the vocabulary-tile partials, then
-// logp, rho and the clipped surrogate; fixed-order block partial sums.
-__global__ __launch_bounds__(kMergeThreads) void merge_loss_kernel(MergeArgs a) {
-  __shared__ double ssum[kMergeThreads];
-  __shared__ long long shi[kMergeThreads], slo[kMergeThreads];
+// 64 action tokens per block.  Each of the 4 waves folds a quarter of the
+// vocabulary-tile partials of its lane's token with the online log-sum-exp
+// update; wave 0 combines the four, then forms logp, rho and the clipped
+// surrogate and writes the block's fixed-order partial sums.
+__global__ __launch_bounds__(256) void merge_loss_kernel(MergeArgs a) {
+  __shared__ f32x2 wpart[4][kMergeRows];
   const int n_act = a.ctrl[0];
-  const int n = blockIdx.x * kMergeThreads + threadIdx.x;
-  double s = 0.0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = blockIdx.x * kMergeRows + lane;
+  float m = -INFINITY, s = 0.0f;
+  if (n < n_act) {
+    for (int t = wave; t < a.tiles_v; t += 4) {
+      const f32x2 p = a.part[(int64_t)t * a.ld_part + n];
+      const float mn = fmaxf(m, p.x);
+      s = s * expf(m - mn) + p.y * expf(p.x - mn);
+      m = mn;
+    }
+  }
+  wpart[wave][lane] = f32x2{m, s};
+  __syncthreads();
+  if (wave != 0) return;
+  double sv = 0.0;
   long long hi = 0, lo = 0;
   if (n < n_act) {
-    float m = -INFINITY;
-    for (int t = 0; t < a.tiles_v; ++t) m = fmaxf(m, a.part[(int64_t)t * a.ld_part + n].x);
+    float mm = -INFINITY;
+    for (int w = 0; w < 4; ++w) mm = fmaxf(mm, wpart[w][lane].x);
     float sum = 0.0f;
-    for (int t = 0; t < a.tiles_v; ++t) {
-      const f32x2 p = a.part[(int64_t)t * a.ld_part + n];
-      if (p.y > 0.0f) sum += p.y * expf(p.x - m);
-    }
-    const float lse = m + logf(sum);
+    for (int w = 0; w < 4; ++w)
+      if (wpart[w][lane].y > 0.0f) sum += wpart[w][lane].y * expf(wpart[w][lane].x - mm);
+    const float lse = mm + logf(sum);
     const float logp = a.zy[n] - lse;
     const float A = a.adv_act[n];
     const float rho = expf(logp - a.old_act[n]);
     const float rc = fminf(fmaxf(rho, 1.0f - a.eps_lo), 1.0f + a.eps_hi);
-    s = (double)fminf(rho * A, rc * A);
+    sv = (double)fminf(rho * A, rc * A);
     hi = (A > 0.0f && rho > 1.0f + a.eps_hi);
     lo = (A < 0.0f && rho < 1.0f - a.eps_lo);
     const int t = a.idx[n];
     a.logp_out[t] = logp;
     a.lse_out[t] = lse;
   }
-  ssum[threadIdx.x] = s;
-  shi[threadIdx.x] = hi;
-  slo[threadIdx.x] = lo;
-  __syncthreads();
-  for (int w = kMergeThreads / 2; w >= 1; w >>= 1) {
-    if (threadIdx.x < w) {
-      ssum[threadIdx.x] += ssum[threadIdx.x + w];
-      shi[threadIdx.x] += shi[threadIdx.x + w];
-      slo[threadIdx.x] += slo[threadIdx.x + w];
-    }
-    __syncthreads();
+  for (int o = 32; o >= 1; o >>= 1) {
+    sv += __shfl_xor(sv, o);
+    hi += __shfl_xor(hi, o);
+    lo += __shfl_xor(lo, o);
   }
-  if (threadIdx.x == 0) {
-    a.blk_sum[blockIdx.x] = ssum[0];
-    a.blk_clip[2 * blockIdx.x] = shi[0];
-    a.blk_clip[2 * blockIdx.x + 1] = slo[0];
+  if (lane == 0) {
+    a.blk_sum[blockIdx.x] = sv;
+    a.blk_clip[2 * blockIdx.x] = hi;
+    a.blk_clip[2 * blockIdx.x + 1] = lo;
   }
 }
 
@@ -380,7 +385,7 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   L->nblk = (int32_t)((T + kScanTile - 1) / kScanTile);
   if (L->nblk < 1) L->nblk = 1;
   L->tiles_v = (int32_t)(L->V_pad / GBN);
-  L->merge_blocks = (int32_t)(L->A_pad / kMergeThreads);
+  L->merge_blocks = (int32_t)(L->A_pad / kMergeRows);
   const int64_t budget = o.g_chunk_bytes > 0 ? o.g_chunk_bytes : kDefaultChunkBytes;
   int64_t vc = budget / (2 * L->A_pad * L->esize) / kRowPad * kRowPad;
   if (vc < kRowPad) vc = kRowPad;
@@ -699,7 +704,7 @@ extern "C" int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32
   m.lse_out = lse;
   m.blk_sum = (double*)(ws + L.blk_sum);
   m.blk_clip = (long long*)(ws + L.blk_clip);
-  hipLaunchKernelGGL(merge_loss_kernel, dim3(L.merge_blocks), dim3(kMergeThreads), 0, s, m);
+  hipLaunchKernelGGL(merge_loss_kernel, dim3(L.merge_blocks), dim3(256), 0, s, m);
   hipLaunchKernelGGL(finalize_loss_kernel, dim3(1), dim3(256), 0, s, L.merge_blocks,
                      (const double*)(ws + L.blk_sum), (const long long*)(ws + L.blk_clip),
                      (const int32_t*)(ws + L.ctrl), n_norm, loss, n_clip);
