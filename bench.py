@@ -95,8 +95,11 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3, help="1..5; 3 is the 32B-shaped batch")
-    ap.add_argument("--cpu-tokens", type=int, default=32,
+    ap.add_argument("--cpu-tokens", type=int, default=128,
                     help="action tokens in the oracle's timed sample (0 skips it)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="before the steps, copy a buffer of this many MiB once (a kernel of known "
+                         "traffic, to scale the HBM counters of a profiling run)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -145,6 +148,15 @@ def main():
                              task_std, adv_traj, adv_tok)
         pl.forward(H, W, token_id, mask, adv_mb, old)
         pl.backward(H, W, token_id, mask, adv_mb, old)
+
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for i in range(Wm):
         step(i)

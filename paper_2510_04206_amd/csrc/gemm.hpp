@@ -6,8 +6,10 @@
 // (v_mfma_f32_32x32x16_bf16 for bf16, v_mfma_f32_32x32x2_f32 for fp32).
 // Each K stage moves 128 bytes of every tile row (64 bf16 or 32 fp32) from
 // global memory straight into LDS (no register staging), double-buffered with
-// one barrier per stage; 16-byte chunks are stored at chunk ^ (row & 7) so the
-// 32-row fragment reads are free of bank conflicts.
+// one barrier per stage.  The 16-byte chunk c of tile row r is stored at chunk
+// c ^ ((r >> 1) & 7): a 128-bit LDS read serves 16 lanes per pass from a
+// 256-byte window (two 128-byte rows), and this places the 16 rows such a pass
+// touches in 16 distinct bank groups.
 //
 // The grid is persistent (about one workgroup per compute unit, since a block
 // holds 128 KiB of LDS).  The row count M and the K extent may be read from
@@ -17,6 +19,8 @@
 // every XCD a contiguous run, and runs are laid out group_m row-tiles deep so
 // the 32 workgroups of an XCD share A and B panels in its L2.
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace agrl {
@@ -78,23 +82,26 @@ __device__ __forceinline__ void map_tile(int t, int grid, int total, int tiles_m
   tn = rem / gsz;
 }
 
+// Swizzle of a tile row: the chunk offset XORed into its 16-byte chunks.
+__device__ __forceinline__ int row_swizzle(int r) { return (r >> 1) & 7; }
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
 // One K stage as direct global -> LDS copies (global_load_lds_dwordx4): each
 // instruction moves 8 tile rows (1 KiB) and writes LDS contiguously, lane i at
-// byte 16 * i.  Lane i therefore fetches logical chunk (i & 7) ^ (row & 7) of
-// row i / 8, which lands it at the swizzled position.  Wave w copies rows
+// byte 16 * i.  Lane i therefore fetches logical chunk (i & 7) ^ row_swizzle(row)
+// of row i / 8, which lands it at the swizzled position.  Wave w copies rows
 // [64 w, 64 w + 64) of both the A and the B tile.  Rows past M or N are clamped
 // to the last valid row (their products are discarded by the epilogue).
 __device__ __forceinline__ void dma_stage(uint8_t* st, const uint8_t* A, int64_t lda_b, int m0,
                                           int M, const uint8_t* B, int64_t ldb_b, int n0, int N,
                                           int64_t k0_b, int wave, int lane) {
   const int rl = lane >> 3;
-  const int c = (lane & 7) ^ rl;
 #pragma unroll
   for (int b = 0; b < 8; ++b) {
     const int r0 = wave * 64 + b * 8;
+    const int c = (lane & 7) ^ row_swizzle(r0 + rl);
     const int64_t ra = min(m0 + r0 + rl, M - 1);
     const int64_t rb = min(n0 + r0 + rl, N - 1);
     __builtin_amdgcn_global_load_lds((glb_void_t*)(A + ra * lda_b + k0_b + c * 16),
@@ -116,7 +123,7 @@ __device__ __forceinline__ void compute_stage(const uint8_t* st, f32x16 (&acc)[4
 template <>
 __device__ __forceinline__ void compute_stage<__bf16>(const uint8_t* st, f32x16 (&acc)[4][4],
                                                       int wm, int wn, int lane) {
-  const int sw = lane & 7;
+  const int sw = row_swizzle(lane & 31);   // fragment rows start at multiples of 32
   const uint8_t* As = st + (wm * 128 + (lane & 31)) * LDS_ROW;
   const uint8_t* Bs = st + GBM * LDS_ROW + (wn * 128 + (lane & 31)) * LDS_ROW;
   bf16x8 a[2][4], b[2][4];
@@ -151,7 +158,7 @@ __device__ __forceinline__ void compute_stage<__bf16>(const uint8_t* st, f32x16 
 template <>
 __device__ __forceinline__ void compute_stage<float>(const uint8_t* st, f32x16 (&acc)[4][4],
                                                      int wm, int wn, int lane) {
-  const int sw = lane & 7;
+  const int sw = row_swizzle(lane & 31);   // fragment rows start at multiples of 32
   const uint8_t* As = st + (wm * 128 + (lane & 31)) * LDS_ROW;
   const uint8_t* Bs = st + GBM * LDS_ROW + (wn * 128 + (lane & 31)) * LDS_ROW;
 #pragma unroll
@@ -225,6 +232,167 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         __syncthreads();
       }
     }
+    epi(acc, m0, n0, tn, M, g.N, smem, wm, wn, lane, tid);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 kernel.  Same tile, waves and swizzle as above, with a software
+// pipeline tuned for one wave per SIMD:
+//   * the per-lane global offsets of the stage copies are computed once per
+//     tile (32-bit, relative to the tile's first row); each stage only moves a
+//     scalar base, so a copy costs one instruction;
+//   * every MFMA of a slice is paired with at most one LDS fragment read or
+//     one stage copy (sched_barrier keeps that order), so the matrix pipe is
+//     never left waiting behind a burst of memory instructions;
+//   * the barrier of stage kt sits before its last 16-deep slice: by then the
+//     slice's fragments are in registers, stage kt+1 has landed and stage kt's
+//     buffer is free, so the last slice's MFMAs cover the barrier, the reads
+//     of stage kt+1's first slice and the copies of stage kt+2 into the freed
+//     buffer.  __syncthreads() is avoided because it would also wait for the
+//     copies still in flight.
+namespace bf16k {
+constexpr int SK = 64;                        // k per stage
+constexpr int ROW = SK * 2;                   // bytes per tile row per stage
+constexpr int STAGE = (GBM + GBN) * ROW;      // 64 KiB
+constexpr int NB = 2;                         // stage buffers
+constexpr int KK = SK / 16;                   // 16-deep slices per stage
+constexpr int RPI = 1024 / ROW;               // tile rows per copy instruction (8)
+constexpr int IPW = 64 / RPI;                 // copy instructions per wave per operand (8)
+constexpr int NCOPY = 2 * IPW;                // per wave per stage (16)
+static_assert(NB * STAGE <= GEMM_LDS, "LDS");
+static_assert(NCOPY == 16, "one copy per MFMA of the last slice");
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+}  // namespace bf16k
+
+template <class Epi>
+__global__ void __launch_bounds__(GEMM_THREADS)
+    __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmShape g, Epi epi) {
+  using namespace bf16k;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[GEMM_LDS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int M = g.m_dev ? *g.m_dev : g.M;
+  const int K = g.k_dev ? cdiv(*g.k_dev, SK) * SK : g.K;
+  if (M <= 0 || g.N <= 0) return;
+  const int tiles_m = cdiv(M, GBM), tiles_n = cdiv(g.N, GBN);
+  const int total = tiles_m * tiles_n;
+  const int nk = K / SK;
+  const int64_t lda_b = g.lda * 2, ldb_b = g.ldb * 2;
+
+  // fragment reads: lane l reads row (l & 31) of each 32-row block, chunk
+  // 2 kk + l / 32 of slice kk
+  const int frow = lane & 31;
+  const int fsw = row_swizzle(frow);
+  const int a_rd = (wm * 128 + frow) * ROW;
+  const int b_rd = GBM * ROW + (wn * 128 + frow) * ROW;
+  int chk[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) chk[kk] = ((kk * 2 + (lane >> 5)) ^ fsw) << 4;
+
+  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+    int tm, tn;
+    map_tile(t, gridDim.x, total, tiles_m, tiles_n, g.group_m, tm, tn);
+    const int m0 = tm * GBM, n0 = tn * GBN;
+    const uint8_t* a_base = (const uint8_t*)g.A + (int64_t)m0 * lda_b;
+    const uint8_t* b_base = (const uint8_t*)g.B + (int64_t)n0 * ldb_b;
+    // copy q < 8 moves A rows [64 wave + 8 q, +8), q >= 8 the same rows of B;
+    // lane i fetches chunk (i & 7) ^ swizzle(row) of row i / 8 (clamped to the
+    // last valid row; those products are discarded by the epilogue)
+    uint32_t offa[IPW], offb[IPW];
+#pragma unroll
+    for (int b = 0; b < IPW; ++b) {
+      const int row = wave * 64 + b * RPI + (lane >> 3);
+      const int ch = ((lane & 7) ^ row_swizzle(row)) << 4;
+      offa[b] = (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
+      offb[b] = (uint32_t)(min(row, g.N - 1 - n0) * ldb_b + ch);
+    }
+    auto copy = [&](int s, int q) {
+      uint8_t* st = smem + (s % NB) * STAGE;
+      const int64_t kb = (int64_t)s * ROW;
+      const int b = q % IPW;
+      const int r0 = wave * 64 + b * RPI;
+      if (q < IPW)
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(a_base + kb + offa[b]),
+                                         (lds_void_t*)(st + r0 * ROW), 16, 0, 0);
+      else
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(b_base + kb + offb[b]),
+                                         (lds_void_t*)(st + GBM * ROW + r0 * ROW), 16, 0, 0);
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    if (nk > 0) {
+      for (int s = 0; s < NB && s < nk; ++s)
+        for (int q = 0; q < NCOPY; ++q) copy(s, q);
+      if (nk >= NB) wait_vmcnt<NCOPY * (NB - 1)>();
+      else wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      bf16x8 fa[2][4], fb[2][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[0][i] = *(const bf16x8*)(smem + a_rd + i * 32 * ROW + chk[0]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) fb[0][j] = *(const bf16x8*)(smem + b_rd + j * 32 * ROW + chk[0]);
+
+      auto stage = [&](int kt, auto refill_c, auto more_c) {
+        constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
+        constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
+        const uint8_t* st = smem + (kt % NB) * STAGE;
+        const uint8_t* sn = smem + ((kt + 1) % NB) * STAGE;
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const int cur = kk & 1, nxt = cur ^ 1;
+          if (kk == KK - 1) {
+            if constexpr (MORE) {
+              if (kt + NB - 1 < nk) wait_vmcnt<NCOPY * (NB - 2)>();
+              else wait_vmcnt<0>();
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+          }
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const int i = q >> 2, j = q & 3;
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
+                                                                0, 0, 0);
+            if (kk < KK - 1) {
+              if (q < 4)
+                fa[nxt][q] = *(const bf16x8*)(st + a_rd + q * 32 * ROW + chk[kk + 1]);
+              else if (q < 8)
+                fb[nxt][q - 4] = *(const bf16x8*)(st + b_rd + (q - 4) * 32 * ROW + chk[kk + 1]);
+            } else {
+              if constexpr (MORE) {
+                if (q < 4)
+                  fa[nxt][q] = *(const bf16x8*)(sn + a_rd + q * 32 * ROW + chk[0]);
+                else if (q < 8)
+                  fb[nxt][q - 4] = *(const bf16x8*)(sn + b_rd + (q - 4) * 32 * ROW + chk[0]);
+              }
+              if constexpr (REFILL) copy(kt + NB, q);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      };
+      int kt = 0;
+      for (; kt + NB < nk; ++kt) stage(kt, std::true_type{}, std::true_type{});
+      for (; kt + 1 < nk; ++kt) stage(kt, std::false_type{}, std::true_type{});
+      stage(kt, std::false_type{}, std::false_type{});
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    __syncthreads();
     epi(acc, m0, n0, tn, M, g.N, smem, wm, wn, lane, tid);
     __syncthreads();
   }

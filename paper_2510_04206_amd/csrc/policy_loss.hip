@@ -458,7 +458,10 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
   if (!W) return bad(AGRL_E_NULL, "W is NULL");
   if (max_act <= 0 || max_act > T) max_act = T;
   // every tile row offset and the G buffers use 32-bit row indices
-  if (round_up(max_act > 0 ? max_act : 1, kRowPad) > ((int64_t)1 << 30)) return bad(AGRL_E_SHAPE, "max_act too large");
+  // operand rows are addressed as 32-bit offsets within a 256-row tile, so a row
+  // of any operand (d, V or the padded action count, in elements) stays below 8M
+  if (round_up(max_act > 0 ? max_act : 1, kRowPad) > ((int64_t)1 << 23)) return bad(AGRL_E_SHAPE, "max_act too large");
+  if (round_up(V, kRowPad) > ((int64_t)1 << 23) || d > (1 << 23)) return bad(AGRL_E_SHAPE, "V or d too large");
   Layout L;
   make_layout(T, max_act, d, V, dtype, o, &L);
   if (T > 0 && (!ws || ws_bytes < L.total)) return bad(AGRL_E_WORKSPACE, "workspace missing or too small");
@@ -485,7 +488,10 @@ void launch_gemm(const GemmShape& g, int max_tiles, const Epi& epi, const agrl_o
   if (max_tiles < grid) grid = max_tiles < 1 ? 1 : max_tiles;
   hipEvent_t* ev = (hipEvent_t*)o.phase_events;
   if (ev) hipEventRecord(ev[2 * ph], s);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g, epi);
+  if constexpr (std::is_same<T, __bf16>::value)
+    hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g, epi);
+  else
+    hipLaunchKernelGGL((gemm_nt_kernel<T, Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g, epi);
   if (ev) hipEventRecord(ev[2 * ph + 1], s);
 }
 
