@@ -71,8 +71,10 @@ typedef struct {
   /* Optional instrumentation: NULL, or a host array of 8 hipEvent_t.  The
    * library records events[2k] on `stream` just before and events[2k+1] just
    * after its matrix-core launch k: 0 forward logits, 1 backward logit
-   * recompute, 2 dW product, 3 dH product (with several vocabulary chunks the
-   * last chunk's launch is the one bracketed). */
+   * recompute, 2 dW product, 3 dH product.  For AGRL_BF16 the dW and dH
+   * products run as one launch, bracketed by events 4/5, and events 6/7 are
+   * recorded back to back.  With several vocabulary chunks the last chunk's
+   * launches are the ones bracketed. */
   void* const* phase_events;
 } agrl_options;
 

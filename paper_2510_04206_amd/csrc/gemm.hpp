@@ -268,22 +268,95 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+
+// One 1 KiB global -> LDS copy (16 bytes per lane, LDS written contiguously
+// from the wave-uniform byte address `lds`).  Issued as inline assembly on
+// purpose: the compiler then does not see an in-flight LDS write, so it does
+// not wait for the copy before later LDS reads of the other stage buffer
+// (its alias analysis cannot tell the buffers apart and would serialise the
+// prefetch).  The kernel orders copies and reads itself: vmcnt wait + barrier
+// before a buffer is read, barrier before it is refilled.  Nothing else in
+// these kernels uses M0.
+__device__ __forceinline__ void copy16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+               : "memory");
+}
 }  // namespace bf16k
+
+// Up to two independent problems in one launch (the backward's dH and dW).
+template <class Epi>
+struct GemmBatch {
+  GemmShape g[2];
+  Epi e[2];
+  int32_t n;          // number of problems
+  int32_t* queue;     // 8 tile counters, zero at launch
+};
+
+// Tile scheduling.  Workgroups are dealt round-robin to the 8 XCDs, so
+// workgroup b serves queue b % nq (nq = 8, fewer for a small grid).  A
+// problem's tiles are ordered 8 row tiles deep, column-major inside a group,
+// and cut into rounds of 32 nq tiles; queue q owns slots [32 q, 32 q + 32) of
+// every round (the final partial round is dealt round-robin).  So at any time
+// all XCDs work on the same few row panels (shared through the Infinity
+// Cache) and each XCD on a compact 8 x 4 block of tiles (shared through its
+// L2), while the workgroups of a queue take its tiles with an atomic counter
+// and balance tiles of unequal length.  Problem 0's tiles come first.
+__device__ __forceinline__ void grouped_tile(int L, int tiles_m, int tiles_n, int group_m,
+                                             int& tm, int& tn) {
+  const int width = group_m * tiles_n;
+  const int grp = L / width;
+  const int first = grp * group_m;
+  const int gsz = min(tiles_m - first, group_m);
+  const int rem = L - grp * width;
+  tm = first + rem % gsz;
+  tn = rem / gsz;
+}
+
+struct QueueShare {
+  int full;     // tiles of this queue in the full rounds
+  int len;      // all tiles of this queue
+};
+
+__device__ __forceinline__ QueueShare queue_share(int total, int q, int nq) {
+  const int round = 32 * nq;
+  const int rounds = total / round;
+  const int tail = total - rounds * round;
+  QueueShare s;
+  s.full = 32 * rounds;
+  s.len = s.full + (tail > q ? (tail - q + nq - 1) / nq : 0);
+  return s;
+}
+
+// k-th tile of queue q -> tile index in the problem's order
+__device__ __forceinline__ int queue_tile(int k, const QueueShare& s, int q, int nq) {
+  if (k < s.full) return (k >> 5) * (32 * nq) + 32 * q + (k & 31);
+  return (s.full / 32) * (32 * nq) + (k - s.full) * nq + q;
+}
 
 template <class Epi>
 __global__ void __launch_bounds__(GEMM_THREADS)
-    __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmShape g, Epi epi) {
+    __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmBatch<Epi> bat) {
   using namespace bf16k;
   __shared__ __attribute__((aligned(16))) uint8_t smem[GEMM_LDS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ int s_tile;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int M = g.m_dev ? *g.m_dev : g.M;
-  const int K = g.k_dev ? cdiv(*g.k_dev, SK) * SK : g.K;
-  if (M <= 0 || g.N <= 0) return;
-  const int tiles_m = cdiv(M, GBM), tiles_n = cdiv(g.N, GBN);
-  const int total = tiles_m * tiles_n;
-  const int nk = K / SK;
-  const int64_t lda_b = g.lda * 2, ldb_b = g.ldb * 2;
+  const int nq = min(8, (int)gridDim.x);
+  const int qi = blockIdx.x % nq;
+  int Mp[2], Kp[2], tmp[2], tnp[2];
+  QueueShare sh[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const GemmShape& gp = bat.g[p];
+    // device-read sizes are the same in every lane; keep them scalar (see below)
+    Mp[p] = __builtin_amdgcn_readfirstlane(gp.m_dev ? *gp.m_dev : gp.M);
+    Kp[p] = __builtin_amdgcn_readfirstlane(gp.k_dev ? cdiv(*gp.k_dev, SK) * SK : gp.K);
+    tmp[p] = cdiv(Mp[p], GBM);
+    tnp[p] = cdiv(gp.N, GBN);
+    const int total = (p < bat.n && Mp[p] > 0 && gp.N > 0) ? tmp[p] * tnp[p] : 0;
+    sh[p] = queue_share(total, qi, nq);
+  }
 
   // fragment reads: lane l reads row (l & 31) of each 32-row block, chunk
   // 2 kk + l / 32 of slice kk
@@ -294,10 +367,26 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   int chk[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) chk[kk] = ((kk * 2 + (lane >> 5)) ^ fsw) << 4;
+  // LDS byte address of the stage buffers
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)smem);
 
-  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+  for (;;) {
+    if (tid == 0) s_tile = atomicAdd(bat.queue + qi, 1);
+    __syncthreads();
+    // the same value in every lane: make it a scalar, otherwise every quantity
+    // derived from it (loop bounds, the copies' LDS base in M0) is treated as
+    // divergent and each copy becomes a waterfall loop
+    const int t = __builtin_amdgcn_readfirstlane(s_tile);
+    if (t >= sh[0].len + sh[1].len) break;
+    const int p = t < sh[0].len ? 0 : 1;
+    const GemmShape g = p ? bat.g[1] : bat.g[0];
+    const Epi epi = p ? bat.e[1] : bat.e[0];
+    const int M = p ? Mp[1] : Mp[0];
+    const int nk = (p ? Kp[1] : Kp[0]) / SK;
     int tm, tn;
-    map_tile(t, gridDim.x, total, tiles_m, tiles_n, g.group_m, tm, tn);
+    const int L = p ? queue_tile(t - sh[0].len, sh[1], qi, nq) : queue_tile(t, sh[0], qi, nq);
+    grouped_tile(L, p ? tmp[1] : tmp[0], p ? tnp[1] : tnp[0], g.group_m, tm, tn);
+    const int64_t lda_b = g.lda * 2, ldb_b = g.ldb * 2;
     const int m0 = tm * GBM, n0 = tn * GBN;
     const uint8_t* a_base = (const uint8_t*)g.A + (int64_t)m0 * lda_b;
     const uint8_t* b_base = (const uint8_t*)g.B + (int64_t)n0 * ldb_b;
@@ -313,16 +402,14 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       offb[b] = (uint32_t)(min(row, g.N - 1 - n0) * ldb_b + ch);
     }
     auto copy = [&](int s, int q) {
-      uint8_t* st = smem + (s % NB) * STAGE;
+      const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE);
       const int64_t kb = (int64_t)s * ROW;
       const int b = q % IPW;
-      const int r0 = wave * 64 + b * RPI;
+      const uint32_t r0 = (uint32_t)(wave * 64 + b * RPI) * ROW;
       if (q < IPW)
-        __builtin_amdgcn_global_load_lds((glb_void_t*)(a_base + kb + offa[b]),
-                                         (lds_void_t*)(st + r0 * ROW), 16, 0, 0);
+        copy16(a_base + kb + offa[b], __builtin_amdgcn_readfirstlane(st + r0));
       else
-        __builtin_amdgcn_global_load_lds((glb_void_t*)(b_base + kb + offb[b]),
-                                         (lds_void_t*)(st + GBM * ROW + r0 * ROW), 16, 0, 0);
+        copy16(b_base + kb + offb[b], __builtin_amdgcn_readfirstlane(st + GBM * ROW + r0));
     };
 
     f32x16 acc[4][4];

@@ -481,18 +481,46 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
 
 enum Phase { PH_FWD = 0, PH_RECOMPUTE = 1, PH_DW = 2, PH_DH = 3 };
 
+__global__ void zero_queue_kernel(int32_t* q) {
+  if (threadIdx.x < 8) q[threadIdx.x] = 0;
+}
+
+// Launch n (1 or 2) independent products.  bf16: one persistent launch of the
+// pipelined kernel with its tile queues reset first; fp32: one simple launch
+// per product.  The phase's events bracket the whole launch (a second phase
+// slot, when given, is recorded empty).
 template <typename T, class Epi>
-void launch_gemm(const GemmShape& g, int max_tiles, const Epi& epi, const agrl_options& o,
-                 Phase ph, hipStream_t s) {
+void launch_gemm(const GemmShape* g, const Epi* e, int n, int max_tiles, int32_t* queue,
+                 const agrl_options& o, Phase ph, int ph2, hipStream_t s) {
   int grid = device_cu_count();
   if (max_tiles < grid) grid = max_tiles < 1 ? 1 : max_tiles;
   hipEvent_t* ev = (hipEvent_t*)o.phase_events;
-  if (ev) hipEventRecord(ev[2 * ph], s);
-  if constexpr (std::is_same<T, __bf16>::value)
-    hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g, epi);
-  else
-    hipLaunchKernelGGL((gemm_nt_kernel<T, Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g, epi);
-  if (ev) hipEventRecord(ev[2 * ph + 1], s);
+  if constexpr (std::is_same<T, __bf16>::value) {
+    GemmBatch<Epi> b;
+    for (int i = 0; i < 2; ++i) {
+      b.g[i] = g[i < n ? i : 0];
+      b.e[i] = e[i < n ? i : 0];
+    }
+    b.n = n;
+    b.queue = queue;
+    hipLaunchKernelGGL(zero_queue_kernel, dim3(1), dim3(64), 0, s, queue);
+    if (ev) hipEventRecord(ev[2 * ph], s);
+    hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, b);
+    if (ev) hipEventRecord(ev[2 * ph + 1], s);
+    if (ev && ph2 >= 0) {
+      hipEventRecord(ev[2 * ph2], s);
+      hipEventRecord(ev[2 * ph2 + 1], s);
+    }
+  } else {
+    for (int i = 0; i < n; ++i) {
+      // with two problems the first is dH (slot ph2) and the second dW (slot ph)
+      const int p = (n == 2 && ph2 >= 0) ? (i == 0 ? ph2 : ph) : ph;
+      if (ev) hipEventRecord(ev[2 * p], s);
+      hipLaunchKernelGGL((gemm_nt_kernel<T, Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, g[i],
+                         e[i]);
+      if (ev) hipEventRecord(ev[2 * p + 1], s);
+    }
+  }
 }
 
 int compact(const Common& c, const Layout& L, uint8_t* ws, const uint8_t* mask,
@@ -559,7 +587,7 @@ void fwd_gemm(const Common& c, const Layout& L, uint8_t* ws, const void* W, hipS
   e.zy = (float*)(ws + L.zy);
   e.scale = c.inv_temp;
   const int max_tiles = (int)(L.A_pad / GBM) * L.tiles_v;
-  launch_gemm<T>(g, max_tiles, e, c.o, PH_FWD, s);
+  launch_gemm<T>(&g, &e, 1, max_tiles, (int32_t*)(ws + L.ctrl + 64), c.o, PH_FWD, -1, s);
 }
 
 template <typename T>
@@ -612,41 +640,40 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       e.ldgt = L.A_pad;
       e.scale = c.inv_temp;
       e.col0 = (int32_t)v0;
-      launch_gemm<T>(g, row_tiles * nv_tiles, e, c.o, PH_RECOMPUTE, s);
+      launch_gemm<T>(&g, &e, 1, row_tiles * nv_tiles, (int32_t*)(ws + L.ctrl + 64), c.o,
+                     PH_RECOMPUTE, -1, s);
     }
-    {  // dW[v0 : v0 + nv] = Gt H_act  (K = action tokens)
-      GemmShape g = {};
-      g.A = Gt;
-      g.lda = L.A_pad;
-      g.B = Ht;
-      g.ldb = L.A_pad;
-      g.M = nv;
-      g.N = c.d;
-      g.k_dev = ctrl;
-      g.group_m = 8;
-      EpiStore e;
-      e.out = dW + v0 * c.d;
-      e.ldo = c.d;
-      e.row_map = nullptr;
-      e.accumulate = c.o.dw_accumulate;
-      launch_gemm<T>(g, nv_tiles * d_tiles, e, c.o, PH_DW, s);
-    }
-    {  // dH[idx] (+)= G W[v0 : v0 + nv]  (K = vocabulary columns of the chunk)
-      GemmShape g = {};
-      g.A = G;
-      g.lda = L.Vc;
-      g.B = Wt + v0;
-      g.ldb = L.V_pad;
-      g.m_dev = ctrl;
-      g.N = c.d;
-      g.K = (int32_t)round_up(nv, KStage<T>::BK);
-      g.group_m = 8;
-      EpiStore e;
-      e.out = dH;
-      e.ldo = c.d;
-      e.row_map = (const int32_t*)(ws + L.idx);
-      e.accumulate = v0 > 0;
-      launch_gemm<T>(g, row_tiles * d_tiles, e, c.o, PH_DH, s);
+    {  // dH[idx] (+)= G W[v0 : v0 + nv] (K = the chunk's vocabulary columns) and
+       // dW[v0 : v0 + nv] = Gt H_act (K = action tokens), one launch, dH first:
+       // its tiles are the long ones
+      GemmShape g[2] = {};
+      g[0].A = G;
+      g[0].lda = L.Vc;
+      g[0].B = Wt + v0;
+      g[0].ldb = L.V_pad;
+      g[0].m_dev = ctrl;
+      g[0].N = c.d;
+      g[0].K = (int32_t)round_up(nv, KStage<T>::BK);
+      g[0].group_m = 8;
+      g[1].A = Gt;
+      g[1].lda = L.A_pad;
+      g[1].B = Ht;
+      g[1].ldb = L.A_pad;
+      g[1].M = nv;
+      g[1].N = c.d;
+      g[1].k_dev = ctrl;
+      g[1].group_m = 8;
+      EpiStore e[2];
+      e[0].out = dH;
+      e[0].ldo = c.d;
+      e[0].row_map = (const int32_t*)(ws + L.idx);
+      e[0].accumulate = v0 > 0;
+      e[1].out = dW + v0 * c.d;
+      e[1].ldo = c.d;
+      e[1].row_map = nullptr;
+      e[1].accumulate = c.o.dw_accumulate;
+      launch_gemm<T>(g, e, 2, row_tiles * d_tiles + nv_tiles * d_tiles,
+                     (int32_t*)(ws + L.ctrl + 64), c.o, PH_DW, PH_DH, s);
     }
   }
 }
