@@ -29,7 +29,13 @@ constexpr int GBM = 256;
 constexpr int GBN = 256;
 constexpr int LDS_ROW = 128;                            // bytes per tile row per stage
 constexpr int STAGE_BYTES = (GBM + GBN) * LDS_ROW;      // 64 KiB
-constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB
+constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB of stage buffers
+// bf16 logit-gradient epilogue: the 256 x 256 tile staged row-major (rows
+// padded to 528 B so the two half-waves of a 16-bit store hit different
+// banks) plus three 256-entry per-row arrays
+constexpr int EPI_ROW = 528;
+constexpr int EPI_STAGE_LDS = GBM * EPI_ROW + 3 * 1024;   // 138240 B
+constexpr int BF16_KERNEL_LDS = EPI_STAGE_LDS > GEMM_LDS ? EPI_STAGE_LDS : GEMM_LDS;
 constexpr int GEMM_THREADS = 256;
 
 template <typename T>
@@ -337,7 +343,7 @@ template <class Epi>
 __global__ void __launch_bounds__(GEMM_THREADS)
     __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmBatch<Epi> bat) {
   using namespace bf16k;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[GEMM_LDS];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[BF16_KERNEL_LDS];
   __shared__ int s_tile;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -488,6 +494,35 @@ __global__ void __launch_bounds__(GEMM_THREADS)
 // ---------------------------------------------------------------------------
 // Epilogues.  Each receives the finished accumulators of one tile.
 
+// Reductions over the 32 lanes of a half-wave (lanes l and l ^ 16, l ^ 8, ...):
+// four DPP steps inside each 16-lane row (xor 1, xor 2 by quad permutes, then
+// the half-row and row mirrors, which pair lanes whose partial results are
+// already uniform within their quad / half-row), then one swizzle across the
+// two rows.  Every lane of the half-wave ends with the result.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                0xF, 0xF, false));
+}
+__device__ __forceinline__ float swz_xor16(float v) {
+  // ds_swizzle bit mode, 32-lane groups: and 0x1F, or 0, xor 0x10
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+__device__ __forceinline__ float half_wave_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));    // quad_perm(1,0,3,2): lane ^ 1
+  v = fmaxf(v, dpp<0x4E>(v));    // quad_perm(2,3,0,1): lane ^ 2
+  v = fmaxf(v, dpp<0x141>(v));   // row_half_mirror: lane i <-> 7 - i within 8
+  v = fmaxf(v, dpp<0x140>(v));   // row_mirror: lane i <-> 15 - i within 16
+  return fmaxf(v, swz_xor16(v));
+}
+__device__ __forceinline__ float half_wave_sum(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x141>(v);
+  v += dpp<0x140>(v);
+  return v + swz_xor16(v);
+}
+
 // Forward: per row of the tile, the max and the sum of exp(z - max) over the
 // tile's vocabulary columns (z = acc / temperature), plus the target logit.
 struct EpiLsePartial {
@@ -519,16 +554,15 @@ struct EpiLsePartial {
           mx = fmaxf(mx, v[j]);
           if (c == target) zy[m0 + rl] = v[j];
         }
-#pragma unroll
-        for (int o = 16; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+        mx = half_wave_max(mx);
+        // a half-row beyond the vocabulary has mx = -inf: its sum is 0
+        const float mref = mx == -INFINITY ? 0.0f : mx;
         float s = 0.0f;
-        if (mx != -INFINITY) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) s += __expf(v[j] - mx);
-        }
-#pragma unroll
-        for (int o = 16; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+        for (int j = 0; j < 4; ++j) s += __expf(v[j] - mref);
+        s = half_wave_sum(s);
         if ((lane & 31) == 0) red[wn * GBM + rl] = f32x2{mx, s};
+        if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
     }
     __syncthreads();
@@ -572,18 +606,31 @@ struct EpiLogitGrad {
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
                                              int N, uint8_t* smem, int wm, int wn, int lane,
                                              int tid) const {
-    int* sy = (int*)smem;
-    float* sl = (float*)(smem + 1024);
-    float* sg = (float*)(smem + 2048);
+    constexpr bool kStage = sizeof(T) == 2;        // bf16: stage G through LDS
+    uint8_t* meta = smem + (kStage ? GBM * EPI_ROW : 0);
+    int* sy = (int*)meta;
+    float* sl = (float*)(meta + 1024);
+    float* sg = (float*)(meta + 2048);
     const bool live = m0 + tid < M;
     sy[tid] = live ? y[m0 + tid] - col0 : -1;
     sl[tid] = live ? lse[m0 + tid] : 0.0f;
     sg[tid] = live ? gs[m0 + tid] : 0.0f;
     __syncthreads();
+    // one group of four rows at a time (sched_barrier bounds the live ranges;
+    // with everything hoisted the epilogue spills), branch-free masking
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
+        int ry[4];
+        float rlse[4], rg[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int rl = acc_row(wm, i, r4 * 4 + q, lane);
+          ry[q] = sy[rl];
+          rlse[q] = sl[rl];
+          rg[q] = sg[rl];
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int cl = acc_col(wn, j, lane);
@@ -593,14 +640,15 @@ struct EpiLogitGrad {
           for (int q = 0; q < 4; ++q) {
             const int r = r4 * 4 + q;
             const int rl = acc_row(wm, i, r, lane);
-            float gval = 0.0f;
-            if (c < N) {
-              const float z = acc[i][j][r] * scale;
-              const float p = __expf(z - sl[rl]);
-              gval = sg[rl] * ((c == sy[rl] ? 1.0f : 0.0f) - p);
-            }
+            const float z = acc[i][j][r] * scale;
+            const float p = __expf(z - rlse[q]);
+            float gval = rg[q] * ((c == ry[q] ? 1.0f : 0.0f) - p);
+            gval = c < N ? gval : 0.0f;
             vals[q] = to_store<T>(gval);
-            G[(int64_t)(m0 + rl) * ldg + c] = vals[q];
+            if constexpr (kStage)
+              *(T*)(smem + rl * EPI_ROW + cl * 2) = vals[q];
+            else
+              G[(int64_t)(m0 + rl) * ldg + c] = vals[q];
           }
           // four consecutive rows of one column: one vector store into Gt
           const int rl0 = acc_row(wm, i, r4 * 4, lane);
@@ -616,6 +664,18 @@ struct EpiLogitGrad {
             *(f32x4*)dst = f32x4{(float)vals[0], (float)vals[1], (float)vals[2], (float)vals[3]};
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if constexpr (kStage) {
+      // the staged tile leaves as full rows: 32 lanes write one row's 512 bytes
+      __syncthreads();
+#pragma unroll 4
+      for (int k = 0; k < GBM * GBN * 2 / (16 * GEMM_THREADS); ++k) {
+        const int qi = tid + GEMM_THREADS * k;
+        const int row = qi >> 5, c16 = qi & 31;
+        const u32x4 v = *(const u32x4*)(smem + row * EPI_ROW + c16 * 16);
+        *(u32x4*)(G + (int64_t)(m0 + row) * ldg + n0 + c16 * 8) = v;
       }
     }
   }
@@ -641,14 +701,16 @@ struct EpiStore {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl = acc_row(wm, i, r, lane);
-        if (m0 + rl >= M) continue;
-        const int64_t orow = row_map ? (int64_t)sr[rl] : (int64_t)(m0 + rl);
-        float* dst = out + orow * ldo;
+        if (m0 + rl < M) {
+          const int64_t orow = row_map ? (int64_t)sr[rl] : (int64_t)(m0 + rl);
+          float* dst = out + orow * ldo;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int c = n0 + acc_col(wn, j, lane);
-          if (c < N) dst[c] = accumulate ? dst[c] + acc[i][j][r] : acc[i][j][r];
+          for (int j = 0; j < 4; ++j) {
+            const int c = n0 + acc_col(wn, j, lane);
+            if (c < N) dst[c] = accumulate ? dst[c] + acc[i][j][r] : acc[i][j][r];
+          }
         }
+        if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
   }
 };
