@@ -17,6 +17,8 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -66,6 +68,37 @@ class HipEvents:
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_sources_digest() -> str:
+    """sha256 over the HIP sources and the build script (counters go stale when these change)."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2510_04206_amd", "csrc", "*")))
+    files.append(os.path.join(ROOT, "paper_2510_04206_amd", "build.py"))
+    for f in files:
+        h.update(os.path.relpath(f, ROOT).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def committed_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` on `workload` from a committed counter summary.
+
+    The summaries under profiles/ carry one line ``traffic-record: {json}`` with
+    the sources digest they were measured on; a record whose digest differs from
+    the current sources is stale and ignored (traffic is then reported as null).
+    """
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as fh:
+            for line in fh:
+                if not line.startswith("traffic-record: "):
+                    continue
+                rec = json.loads(line[len("traffic-record: "):])
+                if (rec.get("workload") == workload and rec.get("kernel") == kernel
+                        and rec.get("sources_sha256") == kernel_sources_digest()):
+                    return rec
+    return None
 
 
 def cpu_baseline(w, adv_tok_host, n_sample, n_act, T):
@@ -187,6 +220,12 @@ def main():
     rates = [f / (ms_ * 1e-3) if f > 0 else 0.0 for f, ms_ in zip(per_launch, phase_ms)]
     dom = int(np.argmax(phase_ms))
     achieved = per_launch[dom] / (phase_ms[dom] * 1e-3)
+    kernel_names = ["gemm_bf16_kernel<EpiLsePartial>", "gemm_bf16_kernel<EpiLogitGrad>",
+                    "gemm_bf16_kernel<EpiStore>", "gemm_bf16_kernel<EpiStore>"]
+    if code != P.AGRL_BF16:
+        kernel_names = [k.replace("gemm_bf16_kernel", "gemm_nt_kernel") for k in kernel_names]
+    dom_kernel = kernel_names[dom]
+    rec = committed_traffic(w.spec.name, dom_kernel + (" grouped" if grouped and dom == 2 else ""))
     step_flops = 4 * gemm_flops
     log("phases (ms): " + ", ".join(f"{n}: {m:.3f}" for n, m in zip(PHASES, phase_ms)))
 
@@ -211,9 +250,12 @@ def main():
         "gemm_ms": dict(zip(["fwd", "recompute", "dW+dH" if grouped else "dW", "dH"], phase_ms)),
         "gemm_tflops": dict(zip(["fwd", "recompute", "dW+dH" if grouped else "dW", "dH"],
                                 [r / 1e12 for r in rates])),
-        "roofline": {"kernel": f"gemm_nt_kernel ({PHASES[dom]})", "bound": "mfma",
+        "roofline": {"kernel": f"{dom_kernel} ({PHASES[dom]})", "bound": "mfma",
                      "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
+                     "frac": achieved / peak,
+                     "traffic": rec["bytes_per_launch"] if rec else None,
+                     "traffic_unit": "bytes per launch (HBM reads + writes, rocprofv3 FETCH_SIZE "
+                                     "and WRITE_SIZE scaled by a copy kernel of known size)",
                      "flops_per_launch": per_launch[dom]},
     }
     if args.cpu_tokens > 0:

@@ -30,11 +30,15 @@ constexpr int GBN = 256;
 constexpr int LDS_ROW = 128;                            // bytes per tile row per stage
 constexpr int STAGE_BYTES = (GBM + GBN) * LDS_ROW;      // 64 KiB
 constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB of stage buffers
-// bf16 logit-gradient epilogue: the 256 x 256 tile staged row-major (rows
-// padded to 528 B so the two half-waves of a 16-bit store hit different
-// banks) plus three 256-entry per-row arrays
-constexpr int EPI_ROW = 528;
-constexpr int EPI_STAGE_LDS = GBM * EPI_ROW + 3 * 1024;   // 138240 B
+// bf16 logit-gradient epilogue (two passes of 128 tile rows): G rows staged
+// row-major with 528-byte pitch (the two half-waves of a 16-bit store land in
+// different banks), the same values transposed as 256 rows of 256 bytes, and
+// three 256-entry per-row arrays
+constexpr int EPI_G_ROW = 528;
+constexpr int EPI_GS = 0;
+constexpr int EPI_GTS = 128 * EPI_G_ROW;                    // 67584
+constexpr int EPI_META = EPI_GTS + 256 * 256;               // 133120
+constexpr int EPI_STAGE_LDS = EPI_META + 3 * 1024;          // 136192 B
 constexpr int BF16_KERNEL_LDS = EPI_STAGE_LDS > GEMM_LDS ? EPI_STAGE_LDS : GEMM_LDS;
 constexpr int GEMM_THREADS = 256;
 
@@ -269,6 +273,7 @@ constexpr int IPW = 64 / RPI;                 // copy instructions per wave per 
 constexpr int NCOPY = 2 * IPW;                // per wave per stage (16)
 static_assert(NB * STAGE <= GEMM_LDS, "LDS");
 static_assert(NCOPY == 16, "one copy per MFMA of the last slice");
+static_assert(NB == 2, "the vmcnt waits assume two stage buffers");
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -287,6 +292,7 @@ __device__ __forceinline__ void copy16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
                : "memory");
 }
+
 }  // namespace bf16k
 
 // Up to two independent problems in one launch (the backward's dH and dW).
@@ -407,6 +413,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       offa[b] = (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
       offb[b] = (uint32_t)(min(row, g.N - 1 - n0) * ldb_b + ch);
     }
+
     auto copy = [&](int s, int q) {
       const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE);
       const int64_t kb = (int64_t)s * ROW;
@@ -429,6 +436,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     if (nk > 0) {
       for (int s = 0; s < NB && s < nk; ++s)
         for (int q = 0; q < NCOPY; ++q) copy(s, q);
+      // stage 0 landed (stage 1's copies may be in flight)
       if (nk >= NB) wait_vmcnt<NCOPY * (NB - 1)>();
       else wait_vmcnt<0>();
       __builtin_amdgcn_s_barrier();
@@ -449,8 +457,8 @@ __global__ void __launch_bounds__(GEMM_THREADS)
           const int cur = kk & 1, nxt = cur ^ 1;
           if (kk == KK - 1) {
             if constexpr (MORE) {
-              if (kt + NB - 1 < nk) wait_vmcnt<NCOPY * (NB - 2)>();
-              else wait_vmcnt<0>();
+              // stage kt+1 landed (its copies are the only ones in flight)
+              wait_vmcnt<0>();
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             __builtin_amdgcn_s_barrier();
@@ -525,6 +533,10 @@ __device__ __forceinline__ float half_wave_sum(float v) {
 
 // Forward: per row of the tile, the max and the sum of exp(z - max) over the
 // tile's vocabulary columns (z = acc / temperature), plus the target logit.
+// A wave reduces its 128 columns for the 16 rows of one accumulator block at
+// a time: 16 independent reduction chains keep the DPP steps free of
+// read-after-write stalls.  With scale > 0, max z = scale * max acc and
+// exp(z - m) = exp2(acc * scale * log2(e) - max acc * scale * log2(e)).
 struct EpiLsePartial {
   const int32_t* y;      // [rows] target id of each compacted row
   f32x2* part;           // [tiles_n][ld_part] (max, sum exp) per row and vocabulary tile
@@ -532,39 +544,100 @@ struct EpiLsePartial {
   float* zy;             // [rows] logit of the target token
   float scale;           // 1 / temperature
 
+  template <bool FULL, int i>
+  __device__ __forceinline__ void block(const f32x16 (&acc)[4][4], int n0, int N,
+                                        const int* sy, f32x2* red, int m0, int wm, int wn,
+                                        int lane) const {
+    const float k1 = scale * 1.44269504088896341f;
+    bool ok[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ok[j] = FULL || n0 + acc_col(wn, j, lane) < N;
+    float mx[16], sm[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float a[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) a[j] = ok[j] ? acc[i][j][r] : -INFINITY;
+      mx[r] = fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3]));
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], dpp<0xB1>(mx[r]));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], dpp<0x4E>(mx[r]));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], dpp<0x141>(mx[r]));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], dpp<0x140>(mx[r]));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], swz_xor16(mx[r]));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      // a half-row beyond the vocabulary has max -inf: its sum is 0
+      const float mk = FULL || mx[r] != -INFINITY ? -mx[r] * k1 : 0.0f;
+      float t = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], k1, mk));
+        t += FULL || ok[j] ? e : 0.0f;
+      }
+      sm[r] = t;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm[r] += dpp<0xB1>(sm[r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm[r] += dpp<0x4E>(sm[r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm[r] += dpp<0x141>(sm[r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm[r] += dpp<0x140>(sm[r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm[r] += swz_xor16(sm[r]);
+    if ((lane & 31) == 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[wn * GBM + acc_row(wm, i, r, lane)] = f32x2{mx[r] * scale, sm[r]};
+    }
+    // target logit: the lane holding the row's target column (if it is one of
+    // this wave's columns) stores it
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = acc_row(wm, i, r, lane);
+      const int tw = sy[rl] - wn * 128 - (lane & 31);    // 32 * block index if held here
+      float v = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v = tw == 32 * j ? acc[i][j][r] : v;
+      if ((unsigned)tw < 128u && (tw & 31) == 0) zy[m0 + rl] = v * scale;
+    }
+  }
+
+  // the block index must be a compile-time constant: a runtime index into
+  // the accumulator array would move it to scratch memory
+  template <bool FULL>
+  __device__ __forceinline__ void blocks(const f32x16 (&acc)[4][4], int n0, int N,
+                                         const int* sy, f32x2* red, int m0, int wm, int wn,
+                                         int lane) const {
+    block<FULL, 0>(acc, n0, N, sy, red, m0, wm, wn, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    block<FULL, 1>(acc, n0, N, sy, red, m0, wm, wn, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    block<FULL, 2>(acc, n0, N, sy, red, m0, wm, wn, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    block<FULL, 3>(acc, n0, N, sy, red, m0, wm, wn, lane);
+  }
+
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
                                              int N, uint8_t* smem, int wm, int wn, int lane,
                                              int tid) const {
     int* sy = (int*)smem;
     f32x2* red = (f32x2*)(smem + 1024);
-    sy[tid] = (m0 + tid < M) ? y[m0 + tid] : -1;
+    // target column relative to the tile (-1: dead row; a target outside the
+    // tile matches no column)
+    sy[tid] = (m0 + tid < M) ? y[m0 + tid] - n0 : -1;
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int rl = acc_row(wm, i, r, lane);
-        const int target = sy[rl];
-        float v[4];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int c = n0 + acc_col(wn, j, lane);
-          v[j] = c < N ? acc[i][j][r] * scale : -INFINITY;
-          mx = fmaxf(mx, v[j]);
-          if (c == target) zy[m0 + rl] = v[j];
-        }
-        mx = half_wave_max(mx);
-        // a half-row beyond the vocabulary has mx = -inf: its sum is 0
-        const float mref = mx == -INFINITY ? 0.0f : mx;
-        float s = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s += __expf(v[j] - mref);
-        s = half_wave_sum(s);
-        if ((lane & 31) == 0) red[wn * GBM + rl] = f32x2{mx, s};
-        if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
-      }
-    }
+    if (n0 + GBN <= N)
+      blocks<true>(acc, n0, N, sy, red, m0, wm, wn, lane);
+    else
+      blocks<false>(acc, n0, N, sy, red, m0, wm, wn, lane);
     __syncthreads();
     const int row = m0 + tid;
     if (row < M) {
@@ -592,7 +665,7 @@ __device__ __forceinline__ float to_store<float>(float v) {
 // written both as G[row][col] and transposed as Gt[col][row].  Rows >= M and
 // columns >= N are written as 0 (they pad the K extent of the next products).
 template <typename T>
-struct EpiLogitGrad {
+struct LogitGradArgs {
   const int32_t* y;
   const float* lse;
   const float* gs;       // dL/dlogp / temperature, per compacted row
@@ -602,80 +675,151 @@ struct EpiLogitGrad {
   int64_t ldgt;
   float scale;
   int32_t col0;          // vocabulary index of this chunk's column 0
+};
 
+template <typename T>
+struct EpiLogitGrad;
+
+// fp32 (simple kernel): direct stores from the accumulator layout.
+template <>
+struct EpiLogitGrad<float> : LogitGradArgs<float> {
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
                                              int N, uint8_t* smem, int wm, int wn, int lane,
                                              int tid) const {
-    constexpr bool kStage = sizeof(T) == 2;        // bf16: stage G through LDS
-    uint8_t* meta = smem + (kStage ? GBM * EPI_ROW : 0);
-    int* sy = (int*)meta;
-    float* sl = (float*)(meta + 1024);
-    float* sg = (float*)(meta + 2048);
+    int* sy = (int*)smem;
+    float* sl = (float*)(smem + 1024);
+    float* sg = (float*)(smem + 2048);
     const bool live = m0 + tid < M;
     sy[tid] = live ? y[m0 + tid] - col0 : -1;
-    sl[tid] = live ? lse[m0 + tid] : 0.0f;
+    sl[tid] = live ? lse[m0 + tid] : INFINITY;
     sg[tid] = live ? gs[m0 + tid] : 0.0f;
     __syncthreads();
-    // one group of four rows at a time (sched_barrier bounds the live ranges;
-    // with everything hoisted the epilogue spills), branch-free masking
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
-        int ry[4];
-        float rlse[4], rg[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int rl = acc_row(wm, i, r4 * 4 + q, lane);
-          ry[q] = sy[rl];
-          rlse[q] = sl[rl];
-          rg[q] = sg[rl];
-        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int cl = acc_col(wn, j, lane);
-          const int c = n0 + cl;
-          T vals[4];
+          const int c = n0 + acc_col(wn, j, lane);
+          float vals[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int r = r4 * 4 + q;
-            const int rl = acc_row(wm, i, r, lane);
-            const float z = acc[i][j][r] * scale;
-            const float p = __expf(z - rlse[q]);
-            float gval = rg[q] * ((c == ry[q] ? 1.0f : 0.0f) - p);
-            gval = c < N ? gval : 0.0f;
-            vals[q] = to_store<T>(gval);
-            if constexpr (kStage)
-              *(T*)(smem + rl * EPI_ROW + cl * 2) = vals[q];
-            else
-              G[(int64_t)(m0 + rl) * ldg + c] = vals[q];
+            const int rl = acc_row(wm, i, r4 * 4 + q, lane);
+            const float p = __expf(acc[i][j][r4 * 4 + q] * scale - sl[rl]);
+            const float g = sg[rl] * ((c == sy[rl] ? 1.0f : 0.0f) - p);
+            vals[q] = c < N ? g : 0.0f;
+            G[(int64_t)(m0 + rl) * ldg + c] = vals[q];
           }
-          // four consecutive rows of one column: one vector store into Gt
           const int rl0 = acc_row(wm, i, r4 * 4, lane);
-          T* dst = Gt + (int64_t)c * ldgt + m0 + rl0;
-          if constexpr (sizeof(T) == 2) {
-            u32x2 packed;
-            packed.x = (uint32_t)__builtin_bit_cast(uint16_t, vals[0]) |
-                       ((uint32_t)__builtin_bit_cast(uint16_t, vals[1]) << 16);
-            packed.y = (uint32_t)__builtin_bit_cast(uint16_t, vals[2]) |
-                       ((uint32_t)__builtin_bit_cast(uint16_t, vals[3]) << 16);
-            *(u32x2*)dst = packed;
-          } else {
-            *(f32x4*)dst = f32x4{(float)vals[0], (float)vals[1], (float)vals[2], (float)vals[3]};
-          }
+          *(f32x4*)(Gt + (int64_t)c * ldgt + m0 + rl0) = f32x4{vals[0], vals[1], vals[2], vals[3]};
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if constexpr (kStage) {
-      // the staged tile leaves as full rows: 32 lanes write one row's 512 bytes
+  }
+};
+
+// bf16 (pipelined kernel).  The tile is finished in two passes of 128 rows
+// (accumulator blocks i = 2h and 2h + 1 of both wave rows).  A pass stages its
+// G rows row-major and the same values transposed (256 rows of 128 bf16, in
+// 8-byte units placed at unit ^ (row & 31) so a wave's transposed stores hit
+// 64 distinct banks), then both leave LDS as full 128-byte lines.  The
+// exponent is evaluated in base 2 with the scale folded in:
+// exp(z - lse) = exp2(acc * scale * log2(e) - lse * log2(e)).
+template <>
+struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
+  template <bool FULL, int h>
+  __device__ __forceinline__ void stage_pass(const f32x16 (&acc)[4][4], int n0, int N,
+                                             uint8_t* smem, int wm, int wn, int lane) const {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    const float k1 = scale * 1.44269504088896341f;
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii) {
+      const int i = 2 * h + ii;
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int rt = acc_row(wm, i, r4 * 4, lane);      // tile row of element q = 0
+        const i32x4 ry = *(const i32x4*)(smem + EPI_META + 4 * rt);
+        const f32x4 rn = *(const f32x4*)(smem + EPI_META + 1024 + 4 * rt);
+        const f32x4 rg = *(const f32x4*)(smem + EPI_META + 2048 + 4 * rt);
+        const int lr = wm * 64 + ii * 32 + 8 * r4 + 4 * (lane >> 5);   // pass-local row
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int cl = acc_col(wn, j, lane);
+          float gv[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r4 * 4 + q], k1, rn[q]));
+            gv[q] = fmaf(-rg[q], p, cl == ry[q] ? rg[q] : 0.0f);
+            if constexpr (!FULL) gv[q] = n0 + cl < N ? gv[q] : 0.0f;
+          }
+          const uint32_t p01 = __builtin_bit_cast(
+              uint32_t, __builtin_convertvector(f32x2{gv[0], gv[1]}, bf16x2_t));
+          const uint32_t p23 = __builtin_bit_cast(
+              uint32_t, __builtin_convertvector(f32x2{gv[2], gv[3]}, bf16x2_t));
+          uint8_t* gs_at = smem + EPI_GS + lr * EPI_G_ROW + cl * 2;
+          *(uint16_t*)(gs_at) = (uint16_t)p01;
+          *(uint16_t*)(gs_at + EPI_G_ROW) = (uint16_t)(p01 >> 16);
+          *(uint16_t*)(gs_at + 2 * EPI_G_ROW) = (uint16_t)p23;
+          *(uint16_t*)(gs_at + 3 * EPI_G_ROW) = (uint16_t)(p23 >> 16);
+          const int unit = (lr >> 2) ^ (cl & 31);
+          *(u32x2*)(smem + EPI_GTS + cl * 256 + unit * 8) = u32x2{p01, p23};
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                             int N, uint8_t* smem, int wm, int wn, int lane,
+                                             int tid) const {
+    {
+      const bool live = m0 + tid < M;
+      // target column relative to the tile, -lse * log2(e) (-inf on dead rows, so
+      // their exponentials are 0 and G is +0 there), dL/dlogp
+      ((int*)(smem + EPI_META))[tid] = live ? y[m0 + tid] - col0 - n0 : -1;
+      ((float*)(smem + EPI_META + 1024))[tid] =
+          live ? -lse[m0 + tid] * 1.44269504088896341f : -INFINITY;
+      ((float*)(smem + EPI_META + 2048))[tid] = live ? gs[m0 + tid] : 0.0f;
+    }
+    __syncthreads();
+    const bool full = n0 + GBN <= N;
+    pass<0>(acc, full, m0, n0, N, smem, wm, wn, lane, tid);
+    __syncthreads();
+    pass<1>(acc, full, m0, n0, N, smem, wm, wn, lane, tid);
+  }
+
+  template <int h>
+  __device__ __forceinline__ void pass(const f32x16 (&acc)[4][4], bool full, int m0, int n0,
+                                       int N, uint8_t* smem, int wm, int wn, int lane,
+                                       int tid) const {
+    {
+      if (full)
+        stage_pass<true, h>(acc, n0, N, smem, wm, wn, lane);
+      else
+        stage_pass<false, h>(acc, n0, N, smem, wm, wn, lane);
       __syncthreads();
+      // G: 128 rows of 512 bytes; pass rows 0..63 are tile rows 64h + r, rows
+      // 64..127 are tile rows 128 + 64h + (r - 64)
 #pragma unroll 4
-      for (int k = 0; k < GBM * GBN * 2 / (16 * GEMM_THREADS); ++k) {
-        const int qi = tid + GEMM_THREADS * k;
-        const int row = qi >> 5, c16 = qi & 31;
-        const u32x4 v = *(const u32x4*)(smem + row * EPI_ROW + c16 * 16);
-        *(u32x4*)(G + (int64_t)(m0 + row) * ldg + n0 + c16 * 8) = v;
+      for (int k = 0; k < 16; ++k) {
+        const int q = tid + GEMM_THREADS * k;
+        const int row = q >> 5, c16 = q & 31;
+        const int trow = 64 * h + (row < 64 ? row : row + 64);
+        const u32x4 v = *(const u32x4*)(smem + EPI_GS + row * EPI_G_ROW + c16 * 16);
+        *(u32x4*)(G + (int64_t)(m0 + trow) * ldg + n0 + c16 * 8) = v;
+      }
+      // Gt: 256 rows (tile columns) of 16 chunks of 8 tile rows each
+#pragma unroll 4
+      for (int k = 0; k < 16; ++k) {
+        const int q = tid + GEMM_THREADS * k;
+        const int row = q >> 4, c16 = q & 15;
+        const int x = row & 31;
+        u32x4 v = *(const u32x4*)(smem + EPI_GTS + row * 256 + (((2 * c16) ^ x) >> 1) * 16);
+        if (x & 1) v = u32x4{v.z, v.w, v.x, v.y};
+        const int trow = 64 * h + (c16 < 8 ? 8 * c16 : 8 * c16 + 64);
+        *(u32x4*)(Gt + (int64_t)(n0 + row) * ldgt + m0 + trow) = v;
       }
     }
   }
