@@ -273,6 +273,17 @@ constexpr int IPW = 64 / RPI;                 // copy instructions per wave per 
 constexpr int NCOPY = 2 * IPW;                // per wave per stage (16)
 static_assert(NB * STAGE <= GEMM_LDS, "LDS");
 static_assert(NCOPY == 16, "one copy per MFMA of the last slice");
+// Copy schedule.  The 16 copies of stage s are spread over the MFMAs that
+// follow the barrier freeing their buffer: MFMA slot 0..15 is the last slice
+// of stage s - 2, slots 16..63 are slices 0..2 of stage s - 1, and copy c
+// (B rows first, then A rows) goes to slot c * CSTRIDE.  Issuing all 16
+// copies of a wave against 16 MFMAs stalls issue when the memory pipeline is
+// backed up, and a stalled wave leaves its matrix pipe idle; copies issued
+// later have less time to land before stage s - 1's barrier.
+constexpr int CSTRIDE = 2;
+static_assert(CSTRIDE >= 1 && 15 * CSTRIDE < 48, "copy schedule");
+__device__ __forceinline__ constexpr int copy_order(int c) { return (c + IPW) % NCOPY; }
+constexpr int NEARLY = (15 / CSTRIDE) + 1;      // copies issued in slot 0..15
 static_assert(NB == 2, "the vmcnt waits assume two stage buffers");
 
 template <int N>
@@ -434,11 +445,14 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     if (nk > 0) {
-      for (int s = 0; s < NB && s < nk; ++s)
-        for (int q = 0; q < NCOPY; ++q) copy(s, q);
-      // stage 0 landed (stage 1's copies may be in flight)
-      if (nk >= NB) wait_vmcnt<NCOPY * (NB - 1)>();
-      else wait_vmcnt<0>();
+      // stage 0 whole; stage 1's slot 0..15 copies (stage 0 issues the rest)
+      for (int q = 0; q < NCOPY; ++q) copy(0, q);
+      if (nk > 1) {
+        for (int c = 0; c < NEARLY; ++c) copy(1, copy_order(c));
+        wait_vmcnt<NEARLY>();      // stage 0 landed
+      } else {
+        wait_vmcnt<0>();
+      }
       __builtin_amdgcn_s_barrier();
       bf16x8 fa[2][4], fb[2][4];
 #pragma unroll
@@ -474,6 +488,11 @@ __global__ void __launch_bounds__(GEMM_THREADS)
                 fa[nxt][q] = *(const bf16x8*)(st + a_rd + q * 32 * ROW + chk[kk + 1]);
               else if (q < 8)
                 fb[nxt][q - 4] = *(const bf16x8*)(st + b_rd + (q - 4) * 32 * ROW + chk[kk + 1]);
+              if constexpr (MORE) {
+                const int slot = 16 * (kk + 1) + q;
+                if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
+                  copy(kt + 1, copy_order(slot / CSTRIDE));
+              }
             } else {
               if constexpr (MORE) {
                 if (q < 4)
@@ -481,7 +500,9 @@ __global__ void __launch_bounds__(GEMM_THREADS)
                 else if (q < 8)
                   fb[nxt][q - 4] = *(const bf16x8*)(sn + b_rd + (q - 4) * 32 * ROW + chk[0]);
               }
-              if constexpr (REFILL) copy(kt + NB, q);
+              if constexpr (REFILL) {
+                if (q % CSTRIDE == 0) copy(kt + NB, copy_order(q / CSTRIDE));
+              }
             }
             __builtin_amdgcn_sched_barrier(0);
           }
