@@ -125,7 +125,7 @@ def cpu_baseline(w, adv_tok_host, n_sample, n_act, T):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3, help="1..5; 3 is the 32B-shaped batch")
     ap.add_argument("--cpu-tokens", type=int, default=128,
@@ -174,13 +174,20 @@ def main():
                       eps_high=w.spec.eps_hi, opt=opt, device=dev)
     log(f"workspace {pl.ws_bytes / 2**30:.2f} GiB")
 
+    # per step: start, advantage normalisation done, end (torch's current stream,
+    # which is the one the library enqueues on)
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K + Wm)]
+
     def step(i):
         opt.phase_events = events.slice_ptr(8 * i)
+        marks[i][0].record()
         B.agrl_task_adv_norm(w.T_g, n_traj, n_task, w.n_group, g_traj, g_mask, traj_task,
                              traj_group, reward, None, act_count, task_count, task_mean,
                              task_std, adv_traj, adv_tok)
+        marks[i][1].record()
         pl.forward(H, W, token_id, mask, adv_mb, old)
         pl.backward(H, W, token_id, mask, adv_mb, old)
+        marks[i][2].record()
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20
@@ -209,16 +216,29 @@ def main():
     if P.agrl_get_device_error() != 0:
         raise RuntimeError("device error flag set during timing")
 
+    step_ms = np.array([marks[i][0].elapsed_time(marks[i][2]) for i in range(Wm, Wm + K)])
+    adv_ms = np.array([marks[i][0].elapsed_time(marks[i][1]) for i in range(Wm, Wm + K)])
+    # advantage normalisation: the count pass and the broadcast each read traj_id and
+    # the mask (5 B per global token); the broadcast writes adv_tok (4 B)
+    adv_bytes = 14.0 * w.T_g
     gemm_flops = 2.0 * n_act * V * d
+    # the backward walks the vocabulary in chunks; its phase events bracket the
+    # last chunk's launches
+    vc = pl.vocab_chunk
+    n_chunks = -(-V // vc)
+    nv_last = V - (n_chunks - 1) * vc
+    chunk_flops = 2.0 * n_act * nv_last * d
     phase_ms = [float(np.mean([events.elapsed_ms(8 * i + 2 * p, 8 * i + 2 * p + 1)
                                for i in range(Wm, Wm + K)])) for p in range(4)]
     peak = PEAK_BF16 if code == P.AGRL_BF16 else PEAK_F32
     # products per bracketed launch: dW and dH share one launch when phase 3 is empty
     grouped = phase_ms[3] < 0.05          # an empty event pair reads a few microseconds
     prods = [1, 1, 2 if grouped else 1, 0 if grouped else 1]
-    per_launch = [gemm_flops * n for n in prods]
+    per_launch = [gemm_flops] + [chunk_flops * n for n in prods[1:]]
     rates = [f / (ms_ * 1e-3) if f > 0 else 0.0 for f, ms_ in zip(per_launch, phase_ms)]
-    dom = int(np.argmax(phase_ms))
+    # the dominant kernel: most time per step (launch time x launches per step)
+    per_step = [phase_ms[0], phase_ms[1] * n_chunks, phase_ms[2] * n_chunks, phase_ms[3] * n_chunks]
+    dom = int(np.argmax(per_step))
     achieved = per_launch[dom] / (phase_ms[dom] * 1e-3)
     kernel_names = ["gemm_bf16_kernel<EpiLsePartial>", "gemm_bf16_kernel<EpiLogitGrad>",
                     "gemm_bf16_kernel<EpiStore>", "gemm_bf16_kernel<EpiStore>"]
@@ -237,16 +257,25 @@ def main():
         "steps": K,
         "warmup": Wm,
         "ms_per_step": ms,
+        "ms_per_step_median": float(np.median(step_ms)),
+        "ms_per_step_min": float(step_ms.min()),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if code == P.AGRL_BF16 else "f32",
         "data": "synthetic",
         "config": {"workload": w.spec.name, "T": T, "N_act": n_act, "V": V, "d": d,
-                   "T_g": w.T_g, "n_traj": n_traj, "n_task": n_task},
+                   "T_g": w.T_g, "n_traj": n_traj, "n_task": n_task,
+                   "vocab_chunk": vc, "vocab_chunks": n_chunks},
         "action_tokens_per_s": n_act / (ms * 1e-3),
+        "model_tflops": 6.0 * n_act * V * d / (ms * 1e-3) / 1e12,
         "mfma_tflops": step_flops / (ms * 1e-3) / 1e12,
         "mfma_frac": step_flops / (ms * 1e-3) / peak,
+        "adv_norm": {"us": float(np.median(adv_ms)) * 1e3,
+                     "GBps": adv_bytes / (float(np.median(adv_ms)) * 1e-3) / 1e9,
+                     "bytes": adv_bytes, "T_g": w.T_g},
+        "gemm_launches_per_step": {"fwd": 1, "recompute": n_chunks,
+                                   "dW+dH" if grouped else "dW": n_chunks},
         "gemm_ms": dict(zip(["fwd", "recompute", "dW+dH" if grouped else "dW", "dH"], phase_ms)),
         "gemm_tflops": dict(zip(["fwd", "recompute", "dW+dH" if grouped else "dW", "dH"],
                                 [r / 1e12 for r in rates])),
@@ -262,6 +291,7 @@ def main():
         adv_host = adv_tok[:T].cpu().numpy()
         log(f"timing the oracle on {args.cpu_tokens} action tokens ...")
         out["cpu_baseline"] = cpu_baseline(w, adv_host, args.cpu_tokens, n_act, T)
+        out["speedup_vs_cpu_baseline"] = out["value"] / out["cpu_baseline"]["value"]
     print(json.dumps(out), flush=True)
 
 

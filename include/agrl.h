@@ -67,7 +67,12 @@ typedef struct {
   float std_eps;         /* added to each std before dividing; 0 selects 1e-6 */
   float temperature;     /* logits are (H W^T) / temperature; 0 selects 1 */
   int32_t dw_accumulate; /* 0: dW is overwritten (default); 1: dW += gradient */
-  int64_t g_chunk_bytes; /* bound on the backward's logit-gradient buffers; 0 selects 32 GiB */
+  /* Bound on the backward's logit-gradient buffers (G and G^T of one vocabulary
+   * chunk, 2 * roundup(max_act, 256) * Vc * element size bytes).  The backward
+   * walks the vocabulary in equal chunks of Vc columns (a multiple of 256), as
+   * few as fit the bound; 0 selects 8 GiB.  The full T x V logit gradient is
+   * held only when it fits the bound. */
+  int64_t g_chunk_bytes;
   /* Optional instrumentation: NULL, or a host array of 8 hipEvent_t.  The
    * library records events[2k] on `stream` just before and events[2k+1] just
    * after its matrix-core launch k: 0 forward logits, 1 backward logit
@@ -123,6 +128,16 @@ int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_gr
  */
 size_t agrl_policy_loss_workspace_size(int64_t T, int64_t max_act, int32_t d, int32_t V,
                                        int32_t dtype, const agrl_options* opt);
+
+/*
+ * Vocabulary columns per backward chunk for these sizes and options (the same
+ * arguments as agrl_policy_loss_workspace_size): a multiple of 256, at most
+ * roundup(V, 256).  The backward recomputes the logits and forms G for
+ * ceil(V / chunk) chunks in order; the last holds the remaining columns.
+ * Returns 0 for invalid sizes.  Host-only; no device work.
+ */
+int64_t agrl_policy_loss_vocab_chunk(int64_t T, int64_t max_act, int32_t d, int32_t V,
+                                     int32_t dtype, const agrl_options* opt);
 
 /*
  * Forward of the token-level clipped policy loss over a packed micro-batch.

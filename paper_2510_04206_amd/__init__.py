@@ -7,9 +7,11 @@ allocates outputs and the workspace with torch.
 """
 from ._binding import (AGRL_BF16, AGRL_F32, AgrlError, agrl_get_device_error,
                        agrl_options, agrl_policy_loss_bwd, agrl_policy_loss_fwd,
-                       agrl_policy_loss_workspace_size, agrl_task_adv_norm, lib)
+                       agrl_policy_loss_vocab_chunk, agrl_policy_loss_workspace_size,
+                       agrl_task_adv_norm, lib)
 from .api import PolicyLoss, task_adv_norm
 
 __all__ = ["AGRL_BF16", "AGRL_F32", "AgrlError", "agrl_options", "agrl_task_adv_norm",
-           "agrl_policy_loss_workspace_size", "agrl_policy_loss_fwd", "agrl_policy_loss_bwd",
+           "agrl_policy_loss_workspace_size", "agrl_policy_loss_vocab_chunk",
+           "agrl_policy_loss_fwd", "agrl_policy_loss_bwd",
            "agrl_get_device_error", "lib", "PolicyLoss", "task_adv_norm"]

@@ -44,6 +44,7 @@ _SIGS = {
     "agrl_task_adv_norm": (_c_i32, [_c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p,
                                     _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "agrl_policy_loss_workspace_size": (_c_sz, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
+    "agrl_policy_loss_vocab_chunk": (_c_i64, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
     "agrl_policy_loss_fwd": (_c_i32, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p,
                                       _c_p, _c_p, _c_p, _c_f32, _c_f32, _c_i64, _c_p, _c_p, _c_sz,
                                       _c_p, _c_p, _c_p, _c_p, _c_p]),
@@ -121,6 +122,10 @@ def agrl_task_adv_norm(T_g, n_traj, n_task, n_group, traj_id, action_mask, traj_
 
 def agrl_policy_loss_workspace_size(T, max_act, d, V, dtype, opt=None) -> int:
     return int(lib().agrl_policy_loss_workspace_size(T, max_act, d, V, dtype, _opts(opt)))
+
+
+def agrl_policy_loss_vocab_chunk(T, max_act, d, V, dtype, opt=None) -> int:
+    return int(lib().agrl_policy_loss_vocab_chunk(T, max_act, d, V, dtype, _opts(opt)))
 
 
 def agrl_policy_loss_fwd(T, max_act, d, V, dtype, H, W, token_id, action_mask, adv_tok, old_logp,

@@ -43,6 +43,9 @@ class PolicyLoss:
         self.opt = B.agrl_options(**opt) if isinstance(opt, dict) else opt
         self.ws_bytes = B.agrl_policy_loss_workspace_size(self.T, self.max_act, self.d, self.V,
                                                           self.code, self.opt)
+        # vocabulary columns per backward chunk (the last chunk holds the rest)
+        self.vocab_chunk = B.agrl_policy_loss_vocab_chunk(self.T, self.max_act, self.d, self.V,
+                                                          self.code, self.opt)
         dev = torch.device(device)
         self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
         self.loss = torch.empty(1, dtype=torch.float32, device=dev)

@@ -370,7 +370,7 @@ struct Layout {
       blk_clip, H_act, part, Ht, Wt, G, Gt, total;
 };
 
-constexpr int64_t kDefaultChunkBytes = (int64_t)32 << 30;
+constexpr int64_t kDefaultChunkBytes = (int64_t)8 << 30;
 
 bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
                  const agrl_options& o, Layout* L) {
@@ -386,10 +386,13 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   if (L->nblk < 1) L->nblk = 1;
   L->tiles_v = (int32_t)(L->V_pad / GBN);
   L->merge_blocks = (int32_t)(L->A_pad / kMergeRows);
+  // vocabulary chunk of the backward: the widest multiple of 256 whose G and G^T
+  // fit the budget, then evened out over the chunks this needs
   const int64_t budget = o.g_chunk_bytes > 0 ? o.g_chunk_bytes : kDefaultChunkBytes;
-  int64_t vc = budget / (2 * L->A_pad * L->esize) / kRowPad * kRowPad;
-  if (vc < kRowPad) vc = kRowPad;
-  L->Vc = vc < L->V_pad ? vc : L->V_pad;
+  int64_t vc_max = budget / (2 * L->A_pad * L->esize) / kRowPad * kRowPad;
+  if (vc_max < kRowPad) vc_max = kRowPad;
+  const int64_t n_chunks = (L->V_pad + vc_max - 1) / vc_max;
+  L->Vc = round_up((V + n_chunks - 1) / n_chunks, kRowPad);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t at = off;
@@ -680,6 +683,16 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
 
 }  // namespace
 }  // namespace agrl
+
+extern "C" int64_t agrl_policy_loss_vocab_chunk(int64_t T, int64_t max_act, int32_t d,
+                                                int32_t V, int32_t dtype,
+                                                const agrl_options* opt) {
+  agrl_options o = {};
+  if (opt) o = *opt;
+  agrl::Layout L;
+  if (T <= 0 || o.g_chunk_bytes < 0 || !agrl::make_layout(T, max_act, d, V, dtype, o, &L)) return 0;
+  return L.Vc;
+}
 
 extern "C" size_t agrl_policy_loss_workspace_size(int64_t T, int64_t max_act, int32_t d,
                                                   int32_t V, int32_t dtype,

@@ -122,6 +122,12 @@ def test_workspace_size(L):
     from paper_2510_04206_amd._binding import agrl_options
     o = agrl_options(g_chunk_bytes=1 << 26)
     assert f(65536, 20000, 5120, 152064, 0, ctypes.byref(o)) < big
+    # default bound: G and G^T of one chunk stay within 8 GiB, so the whole
+    # T x V gradient is never held when it does not fit (64k action rows x 152064
+    # columns x 2 layouts x 2 B = 37 GiB)
+    full = 2 * 65536 * 152064 * 2
+    assert f(65536, 65536, 5120, 152064, 0, None) < full
+    assert f(65536, 65536, 5120, 152064, 0, None) < (8 << 30) + (3 << 30)   # + H_act, H^T, W^T
 
 
 def test_missing_library_fails_loudly(monkeypatch):

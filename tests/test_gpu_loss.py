@@ -73,7 +73,7 @@ def test_vocabulary_chunks_match_single_chunk():
     w = gen.make(gen.small_spec(V=2000, d=128, dtype="bf16", name="chunks"), seed=7)
     g1, _ = _run_case(w)
     A_pad = (w.n_act + 255) // 256 * 256
-    g3, _ = _run_case(w, opt={"g_chunk_bytes": 2 * A_pad * 2 * 768})     # Vc = 768
+    g3, _ = _run_case(w, opt={"g_chunk_bytes": 2 * A_pad * 2 * 768})     # chunks of <= 768 columns
     assert g1["loss"] == g3["loss"]
     np.testing.assert_array_equal(g1["dW"], g3["dW"])                    # dW rows do not mix chunks
     assert rel_fro(g3["dH"], g1["dH"]) < 1e-5
