@@ -216,6 +216,19 @@ def main():
     if P.agrl_get_device_error() != 0:
         raise RuntimeError("device error flag set during timing")
 
+    # the forward-only log-prob pass over the same batch (outside the step)
+    lp = P.TokenLogprob(T, d, V, dtype, max_act=n_act, device=dev)
+    for _ in range(2):
+        lp(H, W, token_id, mask)
+    lp_marks = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for i in range(5):
+        lp_marks[i].record()
+        lp(H, W, token_id, mask)
+    lp_marks[5].record()
+    torch.cuda.synchronize()
+    lp_ms = float(np.median([lp_marks[i].elapsed_time(lp_marks[i + 1]) for i in range(5)]))
+    del lp
+
     step_ms = np.array([marks[i][0].elapsed_time(marks[i][2]) for i in range(Wm, Wm + K)])
     adv_ms = np.array([marks[i][0].elapsed_time(marks[i][1]) for i in range(Wm, Wm + K)])
     # advantage normalisation: the count pass and the broadcast each read traj_id and
@@ -274,6 +287,9 @@ def main():
         "adv_norm": {"us": float(np.median(adv_ms)) * 1e3,
                      "GBps": adv_bytes / (float(np.median(adv_ms)) * 1e-3) / 1e9,
                      "bytes": adv_bytes, "T_g": w.T_g},
+        "logprob_pass": {"ms": lp_ms, "tokens_per_s": T / (lp_ms * 1e-3),
+                         "mfma_frac": 2.0 * n_act * V * d / (lp_ms * 1e-3) / (
+                             PEAK_BF16 if code == P.AGRL_BF16 else PEAK_F32)},
         "gemm_launches_per_step": {"fwd": 1, "recompute": n_chunks,
                                    "dW+dH" if grouped else "dW": n_chunks},
         "gemm_ms": dict(zip(["fwd", "recompute", "dW+dH" if grouped else "dW", "dH"], phase_ms)),

@@ -190,6 +190,29 @@ int agrl_policy_loss_bwd(int64_t T, int64_t max_act, int32_t d, int32_t V, int32
                          const float* logp, float grad_loss, void* workspace, size_t ws_bytes,
                          float* dH, float* dW, void* stream);
 
+/*
+ * Forward-only token log-probabilities over a packed batch: log pi(a_t | s_t)
+ * of every action token, the factorised log-probability of an action
+ * (App. B.1), as needed for the old-policy denominator of the PPO ratio
+ * (App. B.2) when it is recomputed on the trainer rather than taken from the
+ * rollout engine.  The same tiles, partials and merge as agrl_policy_loss_fwd,
+ * so logp and lse are bit-identical to that call's on the same inputs.
+ *
+ *   T, max_act, d, V, dtype, H, W, token_id, action_mask, opt: as for
+ *                   agrl_policy_loss_fwd (opt->temperature divides the logits)
+ *   workspace       at least agrl_token_logprob_workspace_size bytes (the
+ *                   policy-loss workspace also serves)
+ * Outputs:
+ *   logp[T], lse[T] fp32 on action tokens, 0 elsewhere
+ * Errors as for agrl_policy_loss_fwd; T == 0 enqueues nothing.
+ */
+size_t agrl_token_logprob_workspace_size(int64_t T, int64_t max_act, int32_t d, int32_t V,
+                                         int32_t dtype, const agrl_options* opt);
+int agrl_token_logprob(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
+                       const void* H, const void* W, const int32_t* token_id,
+                       const uint8_t* action_mask, const agrl_options* opt, void* workspace,
+                       size_t ws_bytes, float* logp, float* lse, void* stream);
+
 /* Text for a status code (static storage). */
 const char* agrl_status_string(int status);
 

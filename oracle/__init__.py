@@ -120,6 +120,16 @@ def policy_loss(H, W, token_id, mask, adv, old_logp, eps_lo=0.2, eps_hi=0.2, n_n
     return dict(logp=logp, lse=lse, loss=float(loss[0]), n_clip=n_clip, g=g, dH=dH, dW=dW)
 
 
+def token_logprob(H, W, token_id, mask, temperature=1.0, nthreads=None):
+    """log pi(y_t | s_t) and the log-sum-exp of the logits of every action token
+    (App. B.1 token log-probability), 0 elsewhere: the policy-loss forward's
+    logp and lse, which do not depend on advantages or old log-probs."""
+    T = np.asarray(mask).shape[0]
+    r = policy_loss(H, W, token_id, mask, np.zeros(T, np.float32), np.zeros(T, np.float32),
+                    temperature=temperature, backward=False, nthreads=nthreads)
+    return dict(logp=r["logp"], lse=r["lse"])
+
+
 def token_sample(H, W, token_id, mask, adv, old_logp, tokens, eps_lo=0.2, eps_hi=0.2, n_norm=0,
                  temperature=1.0, grad_loss=1.0, dH=True, nthreads=None):
     """lse, logp, g and (optionally) the dH row for the listed token positions only."""

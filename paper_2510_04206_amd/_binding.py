@@ -51,6 +51,9 @@ _SIGS = {
     "agrl_policy_loss_bwd": (_c_i32, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p,
                                       _c_p, _c_p, _c_p, _c_f32, _c_f32, _c_i64, _c_p, _c_p, _c_p,
                                       _c_f32, _c_p, _c_sz, _c_p, _c_p, _c_p]),
+    "agrl_token_logprob_workspace_size": (_c_sz, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
+    "agrl_token_logprob": (_c_i32, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p,
+                                    _c_p, _c_p, _c_sz, _c_p, _c_p, _c_p]),
     "agrl_status_string": (ctypes.c_char_p, [_c_i32]),
     "agrl_last_error": (ctypes.c_char_p, []),
     "agrl_get_device_error": (_c_i32, [_c_p, _c_p]),
@@ -146,6 +149,17 @@ def agrl_policy_loss_bwd(T, max_act, d, V, dtype, H, W, token_id, action_mask, a
         _ptr(adv_tok), _ptr(old_logp), clip_eps_low, clip_eps_high, n_norm, _opts(opt),
         _ptr(lse), _ptr(logp), grad_loss, _ptr(workspace), ws_bytes, _ptr(dH), _ptr(dW),
         _stream(stream)))
+
+
+def agrl_token_logprob_workspace_size(T, max_act, d, V, dtype, opt=None) -> int:
+    return int(lib().agrl_token_logprob_workspace_size(T, max_act, d, V, dtype, _opts(opt)))
+
+
+def agrl_token_logprob(T, max_act, d, V, dtype, H, W, token_id, action_mask, opt, workspace,
+                       ws_bytes, logp, lse, stream=None) -> None:
+    _check("agrl_token_logprob", lib().agrl_token_logprob(
+        T, max_act, d, V, dtype, _ptr(H), _ptr(W), _ptr(token_id), _ptr(action_mask), _opts(opt),
+        _ptr(workspace), ws_bytes, _ptr(logp), _ptr(lse), _stream(stream)))
 
 
 def agrl_get_device_error(stream=None) -> int:

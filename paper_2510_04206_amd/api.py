@@ -69,3 +69,29 @@ class PolicyLoss:
                                self.n_norm, self.opt, self.lse, self.logp, float(grad_loss),
                                self.workspace, self.ws_bytes, self.dH, self.dW, stream)
         return self.dH, self.dW
+
+
+class TokenLogprob:
+    """Forward-only token log-probabilities for one packed-batch shape.
+
+    Holds its workspace and outputs; ``__call__`` returns (logp, lse), fp32 [T],
+    zero on observation tokens.
+    """
+
+    def __init__(self, T: int, d: int, V: int, dtype: torch.dtype, max_act: int = 0, opt=None,
+                 device="cuda"):
+        self.T, self.d, self.V, self.max_act = int(T), int(d), int(V), int(max_act)
+        self.code = B.AGRL_BF16 if dtype == torch.bfloat16 else B.AGRL_F32
+        self.opt = B.agrl_options(**opt) if isinstance(opt, dict) else opt
+        self.ws_bytes = B.agrl_token_logprob_workspace_size(self.T, self.max_act, self.d, self.V,
+                                                            self.code, self.opt)
+        dev = torch.device(device)
+        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self.logp = torch.empty(self.T, dtype=torch.float32, device=dev)
+        self.lse = torch.empty(self.T, dtype=torch.float32, device=dev)
+
+    def __call__(self, H, W, token_id, action_mask, stream=None):
+        B.agrl_token_logprob(self.T, self.max_act, self.d, self.V, self.code, H, W, token_id,
+                             action_mask, self.opt, self.workspace, self.ws_bytes, self.logp,
+                             self.lse, stream)
+        return self.logp, self.lse

@@ -156,8 +156,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_scatter_kernel(ScatterArgs 
     if (ok && pos < a.cap) {
       a.idx[pos] = (int32_t)t;
       a.y_act[pos] = y;
-      const float adv = a.adv_tok[t];
-      const float old = a.old_logp[t];
+      // the forward-only log-prob pass has neither (its merge then forms a zero surrogate)
+      const float adv = a.adv_tok ? a.adv_tok[t] : 0.0f;
+      const float old = a.old_logp ? a.old_logp[t] : 0.0f;
       a.adv_act[pos] = adv;
       a.old_act[pos] = old;
       if (a.gs_act) {
@@ -367,7 +368,7 @@ struct Layout {
   int64_t T, A_pad, V_pad, Vc;
   int32_t d, V, esize, nblk, tiles_v, merge_blocks;
   size_t ctrl, blk_cnt, blk_off, idx, y_act, adv_act, old_act, lse_act, gs_act, zy, blk_sum,
-      blk_clip, H_act, part, Ht, Wt, G, Gt, total;
+      blk_clip, H_act, part, Ht, Wt, G, Gt, fwd_total, total;
 };
 
 constexpr int64_t kDefaultChunkBytes = (int64_t)8 << 30;
@@ -417,6 +418,7 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   const size_t shared_at = off;
   L->part = take((size_t)L->tiles_v * A * 8);
   const size_t fwd_end = off;
+  L->fwd_total = fwd_end;
   off = shared_at;
   L->Ht = take((size_t)d * A * L->esize);
   L->Wt = take((size_t)d * L->V_pad * L->esize);
@@ -437,7 +439,8 @@ struct Common {
 int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
              const void* H, const void* W, const int32_t* token_id, const uint8_t* mask,
              const float* adv, const float* old, float eps_lo, float eps_hi, int64_t n_norm,
-             const agrl_options* opt, void* ws, size_t ws_bytes, Common* c) {
+             const agrl_options* opt, void* ws, size_t ws_bytes, Common* c,
+             bool loss_inputs = true) {
   char buf[200];
   auto bad = [&](int code, const char* what) {
     snprintf(buf, sizeof buf, "%s: %s", fn, what);
@@ -457,7 +460,8 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
     return bad(AGRL_E_FLAGS, "temperature must be finite and >= 0");
   if (o.dw_accumulate != 0 && o.dw_accumulate != 1) return bad(AGRL_E_FLAGS, "dw_accumulate must be 0 or 1");
   if (o.g_chunk_bytes < 0) return bad(AGRL_E_FLAGS, "g_chunk_bytes < 0");
-  if (T > 0 && (!H || !token_id || !mask || !adv || !old)) return bad(AGRL_E_NULL, "input pointer is NULL");
+  if (T > 0 && (!H || !token_id || !mask || (loss_inputs && (!adv || !old))))
+    return bad(AGRL_E_NULL, "input pointer is NULL");
   if (!W) return bad(AGRL_E_NULL, "W is NULL");
   if (max_act <= 0 || max_act > T) max_act = T;
   // every tile row offset and the G buffers use 32-bit row indices
@@ -467,7 +471,8 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
   if (round_up(V, kRowPad) > ((int64_t)1 << 23) || d > (1 << 23)) return bad(AGRL_E_SHAPE, "V or d too large");
   Layout L;
   make_layout(T, max_act, d, V, dtype, o, &L);
-  if (T > 0 && (!ws || ws_bytes < L.total)) return bad(AGRL_E_WORKSPACE, "workspace missing or too small");
+  const size_t need = loss_inputs ? L.total : L.fwd_total;
+  if (T > 0 && (!ws || ws_bytes < need)) return bad(AGRL_E_WORKSPACE, "workspace missing or too small");
   if ((((uintptr_t)H | (uintptr_t)W | (uintptr_t)ws) & 15) != 0)
     return bad(AGRL_E_SHAPE, "H, W and workspace must be 16-byte aligned");
   c->T = T;
@@ -754,6 +759,61 @@ extern "C" int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32
   hipLaunchKernelGGL(finalize_loss_kernel, dim3(1), dim3(256), 0, s, L.merge_blocks,
                      (const double*)(ws + L.blk_sum), (const long long*)(ws + L.blk_clip),
                      (const int32_t*)(ws + L.ctrl), n_norm, loss, n_clip);
+  return hip_status(hipGetLastError());
+}
+
+extern "C" size_t agrl_token_logprob_workspace_size(int64_t T, int64_t max_act, int32_t d,
+                                                    int32_t V, int32_t dtype,
+                                                    const agrl_options* opt) {
+  agrl_options o = {};
+  if (opt) o = *opt;
+  agrl::Layout L;
+  if (T <= 0 || o.g_chunk_bytes < 0 || !agrl::make_layout(T, max_act, d, V, dtype, o, &L)) return 0;
+  return L.fwd_total;
+}
+
+extern "C" int agrl_token_logprob(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
+                                  const void* H, const void* W, const int32_t* token_id,
+                                  const uint8_t* action_mask, const agrl_options* opt,
+                                  void* workspace, size_t ws_bytes, float* logp, float* lse,
+                                  void* stream) {
+  using namespace agrl;
+  Common c;
+  int rc = validate("agrl_token_logprob", T, max_act, d, V, dtype, H, W, token_id, action_mask,
+                    nullptr, nullptr, 0.0f, 0.0f, 0, opt, workspace, ws_bytes, &c, false);
+  if (rc) return rc;
+  if (T > 0 && (!logp || !lse)) return fail(AGRL_E_NULL, "agrl_token_logprob: output pointer is NULL");
+  if (T == 0) return AGRL_OK;
+  hipStream_t s = (hipStream_t)stream;
+  int* err = device_error_ptr();
+  if (!err) return hip_status(hipErrorInvalidSymbol);
+  Layout L;
+  make_layout(T, c.max_act, d, V, dtype, c.o, &L);
+  uint8_t* ws = (uint8_t*)workspace;
+  compact(c, L, ws, action_mask, token_id, nullptr, nullptr, nullptr, nullptr, 0.0f, 0, logp,
+          lse, H, err, s);
+  if (dtype == AGRL_BF16)
+    fwd_gemm<__bf16>(c, L, ws, W, s);
+  else
+    fwd_gemm<float>(c, L, ws, W, s);
+  // the loss merge with zero advantages: lse and logp are formed exactly as in
+  // the policy-loss forward; its (zero) surrogate partials are not finalised
+  MergeArgs m;
+  m.ctrl = (const int32_t*)(ws + L.ctrl);
+  m.tiles_v = L.tiles_v;
+  m.part = (const f32x2*)(ws + L.part);
+  m.ld_part = L.A_pad;
+  m.zy = (const float*)(ws + L.zy);
+  m.old_act = (const float*)(ws + L.old_act);
+  m.adv_act = (const float*)(ws + L.adv_act);
+  m.idx = (const int32_t*)(ws + L.idx);
+  m.eps_lo = 0.0f;
+  m.eps_hi = 0.0f;
+  m.logp_out = logp;
+  m.lse_out = lse;
+  m.blk_sum = (double*)(ws + L.blk_sum);
+  m.blk_clip = (long long*)(ws + L.blk_clip);
+  hipLaunchKernelGGL(merge_loss_kernel, dim3(L.merge_blocks), dim3(256), 0, s, m);
   return hip_status(hipGetLastError());
 }
 

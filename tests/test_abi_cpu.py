@@ -94,6 +94,22 @@ def test_backward_argument_errors(L):
                                   1 << 12, need, 1 << 12, 1 << 12, None) == E_FLAGS
 
 
+def test_token_logprob_argument_errors(L):
+    from paper_2510_04206_amd._binding import agrl_options
+    p = 1 << 12
+    f = L.agrl_token_logprob
+    need = L.agrl_token_logprob_workspace_size(100, 0, 64, 50, 0, None)
+    assert 0 < need < L.agrl_policy_loss_workspace_size(100, 0, 64, 50, 0, None)
+    assert f(100, 0, 64, 50, 7, p, p, p, p, None, p, need, p, p, None) == E_DTYPE
+    assert f(100, 0, 65, 50, 0, p, p, p, p, None, p, need, p, p, None) == E_UNSUP
+    assert f(100, 0, 64, 50, 0, None, p, p, p, None, p, need, p, p, None) == E_NULL
+    assert f(100, 0, 64, 50, 0, p, p, p, p, None, p, need, None, p, None) == E_NULL
+    assert f(100, 0, 64, 50, 0, p, p, p, p, None, p, need - 1, p, p, None) == E_WS
+    o = agrl_options(temperature=float("nan"))
+    assert f(100, 0, 64, 50, 0, p, p, p, p, ctypes.byref(o), p, need, p, p, None) == E_FLAGS
+    assert f(0, 0, 64, 50, 0, None, p, None, None, None, None, 0, None, None, None) == 0
+
+
 def test_adv_norm_argument_errors(L):
     p = 1 << 12
     f = L.agrl_task_adv_norm

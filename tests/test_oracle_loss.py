@@ -292,3 +292,18 @@ def test_decoupled_clip_bounds_hand_placed_ratios(eps):
     assert list(r["n_clip"]) == [int(((A > 0) & (rho > 1 + hi)).sum()),
                                  int(((A < 0) & (rho < 1 - lo)).sum())]
     np.testing.assert_allclose(r["g"], np.where(cut, 0.0, -A * rho / T), rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("temp", [1.0, 0.7])
+def test_token_logprob_against_full_log_softmax(temp):
+    """The forward-only log-prob pass is log_softmax(H W^T / temperature) gathered at
+    the sampled ids on action tokens (torch's log_softmax, fp64), 0 elsewhere."""
+    H, W, y, mask, _, _ = _random_case(50, 333, 24, seed=21)
+    r = oracle.token_logprob(H, W, y, mask, temperature=temp)
+    z = torch.from_numpy(H).double() @ torch.from_numpy(W).double().T / temp
+    ls = torch.log_softmax(z, dim=1)
+    ref = ls[torch.arange(len(y)), torch.from_numpy(y).long()].numpy()
+    m = mask.astype(bool)
+    np.testing.assert_allclose(r["logp"][m], ref[m], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(r["lse"][m], torch.logsumexp(z, 1).numpy()[m], rtol=1e-12)
+    assert np.all(r["logp"][~m] == 0) and np.all(r["lse"][~m] == 0)
