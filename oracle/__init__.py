@@ -91,8 +91,13 @@ def task_adv_norm(traj_id, mask, traj_task, traj_group, reward, n_task, n_group=
 
 
 def policy_loss(H, W, token_id, mask, adv, old_logp, eps_lo=0.2, eps_hi=0.2, n_norm=0,
-                temperature=1.0, grad_loss=1.0, backward=True, nthreads=None):
-    """Whole-batch forward (+ backward): logp, lse, loss, n_clip, g, dH, dW (fp64)."""
+                temperature=1.0, grad_loss=1.0, backward=True, nthreads=None, kl_beta=0.0,
+                kl_estimator=0, ref_logp=None, token_weight=None):
+    """Whole-batch forward (+ backward): logp, lse, loss, n_clip, g, dH, dW (fp64).
+
+    kl_beta / kl_estimator / ref_logp subtract beta * KL(pi || pi_ref) per token
+    (App. A objectives; estimator 0 = k3, 1 = k1); token_weight replaces the
+    1 / N token mean by per-token weights."""
     lib = _load()
     Hn, hb = _as_input(H)
     Wn, wb = _as_input(W)
@@ -108,13 +113,18 @@ def policy_loss(H, W, token_id, mask, adv, old_logp, eps_lo=0.2, eps_hi=0.2, n_n
     n_clip = np.zeros(2, np.int64)
     dH = np.zeros((T, d)) if backward else None
     dW = np.zeros((V, d)) if backward else None
-    f = lib.oracle_policy_loss
+    ref = None if ref_logp is None else np.ascontiguousarray(ref_logp, np.float32)
+    tw = None if token_weight is None else np.ascontiguousarray(token_weight, np.float32)
+    f = lib.oracle_policy_loss_ext
     f.restype = ctypes.c_int
     rc = f(ctypes.c_int64(T), ctypes.c_int32(d), ctypes.c_int32(V), ctypes.c_int32(hb),
            _p(Hn), _p(Wn), _p(y), _p(m), _p(a), _p(o), ctypes.c_double(eps_lo),
            ctypes.c_double(eps_hi), ctypes.c_int64(n_norm), ctypes.c_double(temperature),
-           ctypes.c_double(grad_loss), ctypes.c_int(_threads(nthreads)), _p(logp), _p(lse),
+           ctypes.c_double(grad_loss), ctypes.c_double(kl_beta), ctypes.c_int(kl_estimator),
+           _p(ref), _p(tw), ctypes.c_int(_threads(nthreads)), _p(logp), _p(lse),
            _p(loss), _p(n_clip), _p(g), _p(dH), _p(dW))
+    if rc == -2:
+        raise ValueError("oracle_policy_loss: kl_beta != 0 needs ref_logp")
     if rc != 0:
         raise ValueError("oracle_policy_loss: token id out of range")
     return dict(logp=logp, lse=lse, loss=float(loss[0]), n_clip=n_clip, g=g, dH=dH, dW=dW)

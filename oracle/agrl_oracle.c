@@ -372,18 +372,72 @@ static int64_t* action_rows(int64_t T, const uint8_t* mask, int64_t* count) {
 }
 
 /*
+ * KL penalty of a token against a reference policy (App. A: the PPO and GRPO
+ * objectives subtract beta * D_KL).  With l = logp and r = ref_logp:
+ *   estimator 0 (k3): KL = exp(r - l) - (r - l) - 1,  dKL/dl = 1 - exp(r - l)
+ *   estimator 1 (k1): KL = l - r,                      dKL/dl = 1
+ */
+static double kl_term(double l, double r, int estimator, double* dkl) {
+  if (estimator == 1) {
+    *dkl = 1.0;
+    return l - r;
+  }
+  double u = r - l;
+  *dkl = 1.0 - exp(u);
+  return exp(u) - u - 1.0;
+}
+
+/*
  * Forward (and, when dH/dW are given, backward) over the whole micro-batch.
  * n_norm <= 0 means N_norm = number of action tokens.  Masked tokens are
  * never read; their logp/lse outputs are 0 and their dH rows +0.
  * Outputs: logp[T], lse[T] (fp64), loss, n_clip[2] = {#clip high, #clip low},
  * g[T] = dL/dlogp (nullable), dH[T*d], dW[V*d] (nullable; fp64).
+ *
+ * Extensions (policy_loss_ext): per token f = s - kl_beta * KL(logp, ref_logp)
+ * (KL as in kl_term; kl_beta == 0 leaves the surrogate alone), and per-token
+ * weights w replacing 1 / N_norm when token_weight is given:
+ *   L = -sum_n w_n f_n,   g_n = -grad_loss w_n (ds_n/dlogp - kl_beta dKL_n/dlogp).
  */
+static int policy_loss_impl(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const void* H,
+                            const void* W, const int32_t* y, const uint8_t* mask,
+                            const float* adv, const float* old, double eps_lo, double eps_hi,
+                            int64_t n_norm, double temperature, double grad_loss,
+                            double kl_beta, int kl_estimator, const float* ref_logp,
+                            const float* token_weight, int nthreads, double* logp, double* lse,
+                            double* loss, int64_t* n_clip, double* g, double* dH, double* dW);
+
 int oracle_policy_loss(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const void* H,
                        const void* W, const int32_t* y, const uint8_t* mask, const float* adv,
                        const float* old, double eps_lo, double eps_hi, int64_t n_norm,
                        double temperature, double grad_loss, int nthreads, double* logp,
                        double* lse, double* loss, int64_t* n_clip, double* g, double* dH,
                        double* dW) {
+  return policy_loss_impl(T, d, V, is_bf16, H, W, y, mask, adv, old, eps_lo, eps_hi, n_norm,
+                          temperature, grad_loss, 0.0, 0, NULL, NULL, nthreads, logp, lse, loss,
+                          n_clip, g, dH, dW);
+}
+
+int oracle_policy_loss_ext(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const void* H,
+                           const void* W, const int32_t* y, const uint8_t* mask,
+                           const float* adv, const float* old, double eps_lo, double eps_hi,
+                           int64_t n_norm, double temperature, double grad_loss, double kl_beta,
+                           int kl_estimator, const float* ref_logp, const float* token_weight,
+                           int nthreads, double* logp, double* lse, double* loss,
+                           int64_t* n_clip, double* g, double* dH, double* dW) {
+  if (kl_beta != 0.0 && !ref_logp) return -2;
+  return policy_loss_impl(T, d, V, is_bf16, H, W, y, mask, adv, old, eps_lo, eps_hi, n_norm,
+                          temperature, grad_loss, kl_beta, kl_estimator, ref_logp, token_weight,
+                          nthreads, logp, lse, loss, n_clip, g, dH, dW);
+}
+
+static int policy_loss_impl(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const void* H,
+                            const void* W, const int32_t* y, const uint8_t* mask,
+                            const float* adv, const float* old, double eps_lo, double eps_hi,
+                            int64_t n_norm, double temperature, double grad_loss,
+                            double kl_beta, int kl_estimator, const float* ref_logp,
+                            const float* token_weight, int nthreads, double* logp, double* lse,
+                            double* loss, int64_t* n_clip, double* g, double* dH, double* dW) {
   for (int64_t n = 0; n < T; ++n)
     if (mask[n] && (y[n] < 0 || y[n] >= V)) return -1;
   job_t J;
@@ -406,12 +460,24 @@ int oracle_policy_loss(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const v
   for (int64_t r = 0; r < n_act; ++r) {
     int64_t n = rows[r];
     int clip;
-    sum += surrogate(logp[n], (double)old[n], (double)adv[n], eps_lo, eps_hi,
-                     N > 0 ? grad_loss / N : 0.0, &gg[n], &clip);
+    /* weight of the token: 1/N (applied after the sum) or the caller's w_n */
+    double scale = token_weight ? grad_loss * (double)token_weight[n]
+                                : (N > 0 ? grad_loss / N : 0.0);
+    double f = surrogate(logp[n], (double)old[n], (double)adv[n], eps_lo, eps_hi, scale,
+                         &gg[n], &clip);
+    if (kl_beta != 0.0) {
+      double dkl;
+      f -= kl_beta * kl_term(logp[n], (double)ref_logp[n], kl_estimator, &dkl);
+      gg[n] += scale * kl_beta * dkl;
+    }
+    sum += token_weight ? (double)token_weight[n] * f : f;
     hi += clip == 1;
     lo += clip == -1;
   }
-  *loss = N > 0 ? -sum / N : 0.0;
+  if (token_weight)
+    *loss = -sum;
+  else
+    *loss = N > 0 ? -sum / N : 0.0;
   if (n_clip) {
     n_clip[0] = hi;
     n_clip[1] = lo;

@@ -307,3 +307,108 @@ def test_token_logprob_against_full_log_softmax(temp):
     np.testing.assert_allclose(r["logp"][m], ref[m], rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(r["lse"][m], torch.logsumexp(z, 1).numpy()[m], rtol=1e-12)
     assert np.all(r["logp"][~m] == 0) and np.all(r["lse"][~m] == 0)
+
+
+# ---------------------------------------------------------------------------
+# KL penalty and per-token weights (App. A objectives: -beta * D_KL; sequence-
+# level aggregation as per-token weights)
+
+def _brute_ext(H, W, y, mask, adv, old, eps_lo, eps_hi, beta, est, ref, weight=None):
+    """Full-logit brute force of L = -sum_n w_n (s_n - beta KL_n), w_n = 1/N by default."""
+    z = H.astype(np.float64) @ W.astype(np.float64).T
+    logp = z[np.arange(len(y)), y] - logsumexp(z, axis=1)
+    rho = np.exp(logp - old.astype(np.float64))
+    A = adv.astype(np.float64)
+    s = np.minimum(rho * A, np.clip(rho, 1 - eps_lo, 1 + eps_hi) * A)
+    r = ref.astype(np.float64)
+    kl = (np.exp(r - logp) - (r - logp) - 1.0) if est == 0 else (logp - r)
+    m = mask.astype(bool)
+    w = np.full(len(y), 1.0 / m.sum()) if weight is None else weight.astype(np.float64)
+    return -np.sum((w * (s - beta * kl))[m])
+
+
+@pytest.mark.parametrize("est", [0, 1])
+@pytest.mark.parametrize("beta", [0.05, 0.5])
+def test_kl_loss_against_full_logits(est, beta):
+    H, W, y, mask, adv, old = _random_case(40, 64, 16, seed=31)
+    ref = (old + 0.3 * np.random.default_rng(2).standard_normal(40)).astype(np.float32)
+    r = oracle.policy_loss(H, W, y, mask, adv, old, kl_beta=beta, kl_estimator=est, ref_logp=ref,
+                           backward=False)
+    assert r["loss"] == pytest.approx(_brute_ext(H, W, y, mask, adv, old, 0.2, 0.2, beta, est, ref),
+                                      rel=1e-11)
+
+
+def test_token_weights_against_full_logits():
+    H, W, y, mask, adv, old = _random_case(40, 64, 16, seed=33)
+    w = np.random.default_rng(4).random(40).astype(np.float32)
+    ref = old.copy()
+    r = oracle.policy_loss(H, W, y, mask, adv, old, token_weight=w, kl_beta=0.2, ref_logp=ref,
+                           backward=False)
+    assert r["loss"] == pytest.approx(_brute_ext(H, W, y, mask, adv, old, 0.2, 0.2, 0.2, 0, ref, w),
+                                      rel=1e-11)
+
+
+def test_kl_k3_vanishes_at_the_reference():
+    """ref_logp == logp: k3 KL and its derivative are 0, so everything equals beta = 0."""
+    H, W, y, mask, adv, old = _random_case(30, 50, 12, seed=35)
+    r0 = oracle.policy_loss(H, W, y, mask, adv, old)
+    r1 = oracle.policy_loss(H, W, y, mask, adv, old, kl_beta=0.7, kl_estimator=0,
+                            ref_logp=r0["logp"].astype(np.float32))
+    # ref is logp rounded to fp32: KL ~ (1e-8)^2, gradient ~ 1e-8
+    assert r1["loss"] == pytest.approx(r0["loss"], rel=1e-9, abs=1e-12)
+    np.testing.assert_allclose(r1["g"], r0["g"], rtol=0, atol=1e-8)
+    np.testing.assert_allclose(r1["dH"], r0["dH"], rtol=0, atol=1e-8)
+
+
+def test_kl_k1_adds_a_constant_logp_gradient():
+    """k1: dKL/dlogp = 1, so g gains beta / N on every action token, clipped or not."""
+    H, W, y, mask, adv, old = _random_case(30, 50, 12, seed=37, noise=0.4)
+    ref = np.zeros(30, np.float32)
+    r0 = oracle.policy_loss(H, W, y, mask, adv, old, backward=False)
+    r1 = oracle.policy_loss(H, W, y, mask, adv, old, kl_beta=0.3, kl_estimator=1, ref_logp=ref,
+                            backward=False)
+    m = mask.astype(bool)
+    assert r0["n_clip"].sum() > 0
+    np.testing.assert_allclose(r1["g"][m] - r0["g"][m], 0.3 / m.sum(), rtol=1e-12)
+    assert np.all(r1["g"][~m] == 0)
+
+
+def test_uniform_token_weights_equal_the_token_mean():
+    H, W, y, mask, adv, old = _random_case(30, 50, 12, seed=39)
+    r0 = oracle.policy_loss(H, W, y, mask, adv, old)
+    w = np.full(30, 1.0 / mask.sum(), np.float32)
+    r1 = oracle.policy_loss(H, W, y, mask, adv, old, token_weight=w)
+    # w is 1/N rounded to fp32
+    assert r1["loss"] == pytest.approx(r0["loss"], rel=1e-7)
+    np.testing.assert_allclose(r1["dW"], r0["dW"], rtol=1e-7, atol=1e-14)
+
+
+@pytest.mark.parametrize("est", [0, 1])
+def test_kl_and_weight_gradients_by_finite_differences(est):
+    T, V, d = 20, 13, 5
+    H, W, y, mask, adv, old = _random_case(T, V, d, seed=41, noise=0.2)
+    rng = np.random.default_rng(5)
+    ref = (old + 0.2 * rng.standard_normal(T)).astype(np.float32)
+    w = (0.5 + rng.random(T)).astype(np.float32) / T
+    kw = dict(kl_beta=0.4, kl_estimator=est, ref_logp=ref, token_weight=w, eps_lo=0.2, eps_hi=0.25)
+    base = oracle.policy_loss(H, W, y, mask, adv, old, backward=False, **kw)
+    delta = base["logp"] - old
+    near = (np.abs(delta - math.log(1.25)) < 2e-3) | (np.abs(delta - math.log(0.8)) < 2e-3)
+    mask = (mask.astype(bool) & ~near).astype(np.uint8)
+    full = oracle.policy_loss(H, W, y, mask, adv, old, **kw)
+    L = lambda H_, W_: oracle.policy_loss(H_, W_, y, mask, adv, old, backward=False, **kw)["loss"]
+    h = 1e-3
+    for _ in range(8):
+        n, k = int(rng.integers(T)), int(rng.integers(d))
+        Hp, Hm = H.copy(), H.copy()
+        Hp[n, k] += h
+        Hm[n, k] -= h
+        fd = (L(Hp, W) - L(Hm, W)) / (float(Hp[n, k]) - float(Hm[n, k]))
+        assert fd == pytest.approx(full["dH"][n, k], rel=2e-5, abs=1e-9)
+    for _ in range(8):
+        v, k = int(rng.integers(V)), int(rng.integers(d))
+        Wp, Wm = W.copy(), W.copy()
+        Wp[v, k] += h
+        Wm[v, k] -= h
+        fd = (L(H, Wp) - L(H, Wm)) / (float(Wp[v, k]) - float(Wm[v, k]))
+        assert fd == pytest.approx(full["dW"][v, k], rel=2e-5, abs=1e-9)
