@@ -66,7 +66,10 @@ def _as_input(x):
 
 
 def task_adv_norm(traj_id, mask, traj_task, traj_group, reward, n_task, n_group=0, ddof=0,
-                  eps=1e-6):
+                  eps=1e-6, drop_uniform=False):
+    """Group stage (GRPO, App. B.2) then task stage (Sec. 3.2) in fp32 with the
+    fixed summation order; drop_uniform drops GRPO groups whose rewards are all
+    equal (DAPO dynamic sampling, App. A)."""
     lib = _load()
     traj_id = np.ascontiguousarray(traj_id, np.int32)
     mask = np.ascontiguousarray(mask, np.uint8)
@@ -78,13 +81,15 @@ def task_adv_norm(traj_id, mask, traj_task, traj_group, reward, n_task, n_group=
     out = dict(act_count=np.zeros(n_traj, np.int32), task_count=np.zeros(n_task, np.int64),
                task_mean=np.zeros(n_task, np.float32), task_std=np.zeros(n_task, np.float32),
                adv_traj=np.zeros(n_traj, np.float32), adv_tok=np.zeros(T_g, np.float32))
-    f = lib.oracle_task_adv_norm
+    f = lib.oracle_task_adv_norm_ext
     f.restype = ctypes.c_int
     rc = f(ctypes.c_int64(T_g), ctypes.c_int32(n_traj), ctypes.c_int32(n_task),
            ctypes.c_int32(n_group), _p(traj_id), _p(mask), _p(traj_task), _p(traj_group),
-           _p(reward), ctypes.c_int32(ddof), ctypes.c_float(eps), _p(out["act_count"]),
-           _p(out["task_count"]), _p(out["task_mean"]), _p(out["task_std"]),
+           _p(reward), ctypes.c_int32(ddof), ctypes.c_float(eps), ctypes.c_int32(int(drop_uniform)),
+           _p(out["act_count"]), _p(out["task_count"]), _p(out["task_mean"]), _p(out["task_std"]),
            _p(out["adv_traj"]), _p(out["adv_tok"]))
+    if rc == -2:
+        raise ValueError("oracle_task_adv_norm: drop_uniform needs groups")
     if rc != 0:
         raise ValueError("oracle_task_adv_norm: id out of range")
     return out

@@ -80,12 +80,50 @@ static float csum64(const float* x, const unsigned char* sel, int64_t n) {
  *    gives sigma = 0.
  * 4. adv_tok[t] = A_tilde of traj_id[t] on action tokens, 0 elsewhere.
  */
+static int task_adv_norm_impl(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_group,
+                              const int32_t* traj_id, const uint8_t* mask,
+                              const int32_t* traj_task, const int32_t* traj_group,
+                              const float* reward, int32_t ddof, float eps, int32_t drop_uniform,
+                              int32_t* act_count, int64_t* task_count, float* task_mean,
+                              float* task_std, float* adv_traj, float* adv_tok);
+
 int oracle_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_group,
                          const int32_t* traj_id, const uint8_t* mask,
                          const int32_t* traj_task, const int32_t* traj_group,
                          const float* reward, int32_t ddof, float eps,
                          int32_t* act_count, int64_t* task_count, float* task_mean,
                          float* task_std, float* adv_traj, float* adv_tok) {
+  return task_adv_norm_impl(T_g, n_traj, n_task, n_group, traj_id, mask, traj_task, traj_group,
+                            reward, ddof, eps, 0, act_count, task_count, task_mean, task_std,
+                            adv_traj, adv_tok);
+}
+
+/*
+ * With drop_uniform (DAPO's dynamic sampling, App. A: groups whose responses
+ * are all correct or all incorrect carry no signal and are filtered out), a
+ * GRPO group whose rewards are all equal (exact fp32 equality; a group of one
+ * is such a group) is dropped: its trajectories get advantage 0 and their
+ * tokens are left out of the task statistics (N_i, mu_i, sigma_i).
+ * act_count still counts every trajectory's action tokens.
+ */
+int oracle_task_adv_norm_ext(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_group,
+                             const int32_t* traj_id, const uint8_t* mask,
+                             const int32_t* traj_task, const int32_t* traj_group,
+                             const float* reward, int32_t ddof, float eps, int32_t drop_uniform,
+                             int32_t* act_count, int64_t* task_count, float* task_mean,
+                             float* task_std, float* adv_traj, float* adv_tok) {
+  if (drop_uniform && !traj_group) return -2;
+  return task_adv_norm_impl(T_g, n_traj, n_task, n_group, traj_id, mask, traj_task, traj_group,
+                            reward, ddof, eps, drop_uniform, act_count, task_count, task_mean,
+                            task_std, adv_traj, adv_tok);
+}
+
+static int task_adv_norm_impl(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_group,
+                              const int32_t* traj_id, const uint8_t* mask,
+                              const int32_t* traj_task, const int32_t* traj_group,
+                              const float* reward, int32_t ddof, float eps, int32_t drop_uniform,
+                              int32_t* act_count, int64_t* task_count, float* task_mean,
+                              float* task_std, float* adv_traj, float* adv_tok) {
   for (int32_t j = 0; j < n_traj; ++j) act_count[j] = 0;
   for (int64_t t = 0; t < T_g; ++t) {
     if (traj_id[t] >= n_traj) return -1;
@@ -99,6 +137,7 @@ int oracle_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_
   float* a_hat = (float*)malloc(sizeof(float) * (size_t)(n_traj > 0 ? n_traj : 1));
   float* term = (float*)malloc(sizeof(float) * (size_t)(n_traj > 0 ? n_traj : 1));
   unsigned char* sel = (unsigned char*)malloc((size_t)(n_traj > 0 ? n_traj : 1));
+  unsigned char* dropped = (unsigned char*)calloc((size_t)(n_traj > 0 ? n_traj : 1), 1);
 
   /* group stage */
   if (traj_group) {
@@ -109,6 +148,28 @@ int oracle_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_
         K += sel[j];
       }
       if (K == 0) continue;
+      if (drop_uniform) {
+        int uniform = 1;
+        float r0 = 0.0f;
+        int seen = 0;
+        for (int32_t j = 0; j < n_traj; ++j) {
+          if (!sel[j]) continue;
+          if (!seen) {
+            r0 = reward[j];
+            seen = 1;
+          } else if (reward[j] != r0) {
+            uniform = 0;
+          }
+        }
+        if (uniform) {
+          for (int32_t j = 0; j < n_traj; ++j)
+            if (sel[j]) {
+              dropped[j] = 1;
+              a_hat[j] = 0.0f;
+            }
+          continue;
+        }
+      }
       if (K - ddof <= 0) {
         for (int32_t j = 0; j < n_traj; ++j)
           if (sel[j]) a_hat[j] = 0.0f;
@@ -132,7 +193,7 @@ int oracle_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_
   for (int32_t i = 0; i < n_task; ++i) {
     int64_t N = 0;
     for (int32_t j = 0; j < n_traj; ++j) {
-      sel[j] = (traj_task[j] == i);
+      sel[j] = (traj_task[j] == i) && !dropped[j];
       if (sel[j]) N += act_count[j];
     }
     task_count[i] = N;
@@ -157,6 +218,8 @@ int oracle_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_
     for (int32_t j = 0; j < n_traj; ++j)
       if (sel[j]) adv_traj[j] = f_div(f_sub(a_hat[j], mu), den);
   }
+  for (int32_t j = 0; j < n_traj; ++j)
+    if (dropped[j]) adv_traj[j] = 0.0f;
 
   if (adv_tok)
     for (int64_t t = 0; t < T_g; ++t)
@@ -165,6 +228,7 @@ int oracle_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_
   free(a_hat);
   free(term);
   free(sel);
+  free(dropped);
   return 0;
 }
 

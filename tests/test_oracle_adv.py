@@ -29,7 +29,8 @@ def test_golden_closed_forms(case):
                                np.array(case["traj_task"]),
                                None if tg is None else np.array(tg),
                                np.array(case["reward"], np.float32), case["n_task"],
-                               case["n_group"], ddof=case["ddof"])
+                               case["n_group"], ddof=case["ddof"],
+                               drop_uniform=case.get("drop_uniform", False))
     exp = case["expect"]
     exact = set(exp.get("exact", []))
     for key in ("act_count", "task_count"):
@@ -76,14 +77,18 @@ def test_counts_brute_force(k):
     np.testing.assert_array_equal(out["adv_tok"], want)
 
 
-def _fp64_reference(w, ddof=0, eps=1e-6, groups=True):
+def _fp64_reference(w, ddof=0, eps=1e-6, groups=True, drop_uniform=False, reward=None):
     """The two normalisation stages written with numpy fp64 reductions."""
-    R = w.reward.astype(np.float64)
+    R = (w.reward if reward is None else reward).astype(np.float64)
+    keep = np.ones(len(R), bool)
     if groups:
         A = np.zeros_like(R)
         for g in range(w.n_group):
             s = w.traj_group == g
             K = s.sum()
+            if drop_uniform and K > 0 and np.all(R[s] == R[s][0]):
+                keep[s] = False
+                continue
             if K - ddof <= 0:
                 continue
             mu = R[s].mean()
@@ -95,7 +100,7 @@ def _fp64_reference(w, ddof=0, eps=1e-6, groups=True):
     n = np.bincount(w.g_traj_id[sel], minlength=w.n_traj).astype(np.float64)
     out = np.zeros_like(R)
     for i in range(w.n_task):
-        s = w.traj_task == i
+        s = (w.traj_task == i) & keep
         N = n[s].sum()
         if N == 0:
             continue
@@ -116,6 +121,29 @@ def test_fp32_against_fp64(k, groups):
     ref = _fp64_reference(w, groups=groups)
     # fp32 rounding of O(1) quantities, amplified at most by 1/sigma of the task
     np.testing.assert_allclose(out["adv_traj"], ref, rtol=2e-5, atol=2e-5)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 5])
+def test_drop_uniform_groups_against_fp64(k):
+    """DAPO dynamic sampling: planted all-equal groups are dropped (advantage 0,
+    left out of the task statistics); the rest matches the fp64 formulation."""
+    w = gen.config(k, tensors=False)
+    R = w.reward.copy()
+    rng = np.random.default_rng(k)
+    for g in rng.choice(w.n_group, size=max(1, w.n_group // 4), replace=False):
+        R[w.traj_group == g] = R[w.traj_group == g][0]
+    out = oracle.task_adv_norm(w.g_traj_id, w.g_mask, w.traj_task, w.traj_group, R, w.n_task,
+                               w.n_group, drop_uniform=True)
+    ref = _fp64_reference(w, drop_uniform=True, reward=R)
+    np.testing.assert_allclose(out["adv_traj"], ref, rtol=2e-5, atol=2e-5)
+    dropped = np.zeros(w.n_traj, bool)
+    for g in range(w.n_group):
+        s = w.traj_group == g
+        dropped[s] = np.all(R[s] == R[s][0])
+    assert dropped.any() and np.all(out["adv_traj"][dropped] == 0)
+    n = np.bincount(w.g_traj_id[(w.g_mask == 1) & (w.g_traj_id >= 0)], minlength=w.n_traj)
+    for i in range(w.n_task):
+        assert out["task_count"][i] == n[(w.traj_task == i) & ~dropped].sum()
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
