@@ -81,6 +81,25 @@ typedef struct {
    * recorded back to back.  With several vocabulary chunks the last chunk's
    * launches are the ones bracketed. */
   void* const* phase_events;
+  /* KL penalty against a reference policy (App. A: the PPO and GRPO
+   * objectives subtract beta * D_KL).  Per action token, with l = logp and
+   * r = ref_logp[t]: kl_estimator 0 (k3, default) KL = exp(r - l) - (r - l) - 1,
+   * 1 (k1) KL = l - r.  The loss uses s - kl_beta * KL in place of the
+   * surrogate s.  kl_beta = 0 disables it; otherwise ref_logp is a device
+   * array of T fp32 values, read on action tokens. */
+  float kl_beta;
+  int32_t kl_estimator;
+  const float* ref_logp;
+  /* Per-token loss weights (device, T fp32, read on action tokens): the loss
+   * becomes L = -sum_t w_t (s_t - kl_beta KL_t) in place of the token mean
+   * -(1/N) sum_t (...), and n_norm is ignored.  Sequence-level aggregation
+   * (App. B.2's GRPO form: a token mean per trajectory, then a mean over
+   * trajectories) is w_t = 1 / (n_seq * n_traj(t)).  NULL: token mean. */
+  const float* token_weight;
+  /* agrl_task_adv_norm only: 1 drops every GRPO group whose rewards are all
+   * equal (App. A, DAPO's dynamic sampling): its trajectories get advantage 0
+   * and are left out of the task statistics.  Needs traj_group. */
+  int32_t drop_uniform_groups;
 } agrl_options;
 
 /*

@@ -29,7 +29,10 @@ _c_i64, _c_i32, _c_f32, _c_p, _c_sz = (ctypes.c_int64, ctypes.c_int32, ctypes.c_
 class agrl_options(ctypes.Structure):
     _fields_ = [("std_ddof", ctypes.c_int32), ("std_eps", ctypes.c_float),
                 ("temperature", ctypes.c_float), ("dw_accumulate", ctypes.c_int32),
-                ("g_chunk_bytes", ctypes.c_int64), ("phase_events", ctypes.c_void_p)]
+                ("g_chunk_bytes", ctypes.c_int64), ("phase_events", ctypes.c_void_p),
+                ("kl_beta", ctypes.c_float), ("kl_estimator", ctypes.c_int32),
+                ("ref_logp", ctypes.c_void_p), ("token_weight", ctypes.c_void_p),
+                ("drop_uniform_groups", ctypes.c_int32)]
 
 
 class AgrlError(RuntimeError):

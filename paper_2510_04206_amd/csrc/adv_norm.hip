@@ -78,10 +78,14 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 }
 
 // GRPO stage: one wave per group.  Lane l owns trajectories l, l+64, ...
+// With drop_uniform, a group whose rewards are all equal is marked dropped by a
+// quiet NaN in a_hat (the task stage leaves such trajectories out and gives
+// them advantage 0).
 __global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_traj,
                                                     const int32_t* __restrict__ traj_group,
                                                     const float* __restrict__ reward,
-                                                    int32_t ddof, float eps, float* a_hat) {
+                                                    int32_t ddof, float eps, int32_t drop_uniform,
+                                                    float* a_hat) {
   const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (g >= n_group) return;
   const int lane = threadIdx.x & 63;
@@ -94,6 +98,24 @@ __global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_t
     K += __popcll(__ballot(mem));
   }
   if (K == 0) return;
+  if (drop_uniform) {
+    // exact: min and max over the members do not depend on the order
+    float lo = INFINITY, hi = -INFINITY;
+    for (int tau = lane; tau < n_traj; tau += 64)
+      if (traj_group[tau] == g) {
+        lo = fminf(lo, reward[tau]);
+        hi = fmaxf(hi, reward[tau]);
+      }
+    for (int o = 32; o >= 1; o >>= 1) {
+      lo = fminf(lo, __shfl_xor(lo, o));
+      hi = fmaxf(hi, __shfl_xor(hi, o));
+    }
+    if (lo == hi) {
+      for (int tau = lane; tau < n_traj; tau += 64)
+        if (traj_group[tau] == g) a_hat[tau] = __builtin_nanf("");
+      return;
+    }
+  }
   if (K - ddof <= 0) {
     for (int tau = lane; tau < n_traj; tau += 64)
       if (traj_group[tau] == g) a_hat[tau] = 0.0f;
@@ -116,19 +138,25 @@ __global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_t
 // Task stage: one wave per task; statistics of the token-level set, where
 // trajectory tau contributes its advantage with multiplicity n_tau.
 // src may alias adv_traj: each lane reads its own trajectories before writing them.
+// With drop_uniform, trajectories whose group stage left a NaN mark (dropped
+// groups) are not members of their task's set and get advantage 0.
 __global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_traj,
                                                    const int32_t* __restrict__ traj_task,
                                                    const int32_t* __restrict__ act_count,
                                                    const float* src, int32_t ddof, float eps,
-                                                   int64_t* task_count, float* task_mean,
-                                                   float* task_std, float* adv_traj) {
+                                                   int32_t drop_uniform, int64_t* task_count,
+                                                   float* task_mean, float* task_std,
+                                                   float* adv_traj) {
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= n_task) return;
   const int lane = threadIdx.x & 63;
+  auto member = [&](int tau) {
+    return traj_task[tau] == i && !(drop_uniform && isnan(src[tau]));
+  };
   float acc = 0.0f;
   int64_t n_lane = 0;
   for (int tau = lane; tau < n_traj; tau += 64) {
-    if (traj_task[tau] == i) {
+    if (member(tau)) {
       const int n = act_count[tau];
       n_lane += n;
       acc = acc + (float)n * src[tau];
@@ -137,7 +165,7 @@ __global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_tra
   const int64_t N = wave_sum_i64(n_lane);
   if (N == 0) {
     for (int tau = lane; tau < n_traj; tau += 64)
-      if (traj_task[tau] == i) adv_traj[tau] = 0.0f;
+      if (traj_task[tau] == i) adv_traj[tau] = 0.0f;       // dropped ones included
     if (lane == 0) {
       task_count[i] = 0;
       task_mean[i] = 0.0f;
@@ -148,7 +176,7 @@ __global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_tra
   const float mu = butterfly_sum(acc) / (float)N;
   acc = 0.0f;
   for (int tau = lane; tau < n_traj; tau += 64) {
-    if (traj_task[tau] == i) {
+    if (member(tau)) {
       const float dv = src[tau] - mu;
       acc = acc + (float)act_count[tau] * (dv * dv);
     }
@@ -157,7 +185,7 @@ __global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_tra
   const float sigma = (N - ddof > 0) ? sqrtf(q / (float)(N - ddof)) : 0.0f;
   const float den = sigma + eps;
   for (int tau = lane; tau < n_traj; tau += 64)
-    if (traj_task[tau] == i) adv_traj[tau] = (src[tau] - mu) / den;
+    if (traj_task[tau] == i) adv_traj[tau] = member(tau) ? (src[tau] - mu) / den : 0.0f;
   if (lane == 0) {
     task_count[i] = N;
     task_mean[i] = mu;
@@ -208,6 +236,10 @@ extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, i
   if (!(o.std_eps >= 0.0f) || !isfinite(o.std_eps))
     return fail(AGRL_E_FLAGS, "agrl_task_adv_norm: std_eps must be finite and >= 0");
   const float eps = o.std_eps == 0.0f ? 1e-6f : o.std_eps;
+  if (o.drop_uniform_groups != 0 && o.drop_uniform_groups != 1)
+    return fail(AGRL_E_FLAGS, "agrl_task_adv_norm: drop_uniform_groups must be 0 or 1");
+  if (o.drop_uniform_groups && !traj_group && n_traj > 0)
+    return fail(AGRL_E_FLAGS, "agrl_task_adv_norm: drop_uniform_groups needs traj_group");
 
   hipStream_t s = (hipStream_t)stream;
   int* err = device_error_ptr();
@@ -226,11 +258,13 @@ extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, i
   }
   if (traj_group && n_group > 0)
     hipLaunchKernelGGL(group_kernel, dim3(cdiv(n_group, 4)), dim3(256), 0, s, n_group, n_traj,
-                       traj_group, reward, (int32_t)o.std_ddof, eps, adv_traj);
+                       traj_group, reward, (int32_t)o.std_ddof, eps, o.drop_uniform_groups,
+                       adv_traj);
   if (n_task > 0)
     hipLaunchKernelGGL(task_kernel, dim3(cdiv(n_task, 4)), dim3(256), 0, s, n_task, n_traj,
                        traj_task, act_count, traj_group ? (const float*)adv_traj : reward,
-                       (int32_t)o.std_ddof, eps, task_count, task_mean, task_std, adv_traj);
+                       (int32_t)o.std_ddof, eps, traj_group ? o.drop_uniform_groups : 0, task_count,
+                       task_mean, task_std, adv_traj);
   if (adv_tok && T_g > 0)
     hipLaunchKernelGGL(broadcast_kernel, dim3((unsigned)cdiv<int64_t>(T_g, 256)), dim3(256), 0, s,
                        T_g, n_traj, traj_id, action_mask, (const float*)adv_traj, adv_tok);

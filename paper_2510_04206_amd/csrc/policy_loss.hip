@@ -111,6 +111,12 @@ struct ScatterArgs {
   float* gs_act;            // backward only: dL/dlogp / temperature
   float* logp_out;          // forward only: zeroed on masked tokens
   float* lse_out;
+  const float* ref_logp;    // nullable: reference log-probs of the KL penalty
+  const float* token_weight;  // nullable: per-token loss weights
+  float* ref_act;           // forward only: compacted ref_logp / weights
+  float* w_act;
+  float kl_beta;
+  int32_t kl_est;
   float eps_lo, eps_hi;
   float grad_loss;
   int64_t n_norm;
@@ -162,14 +168,24 @@ __global__ __launch_bounds__(kScanThreads) void scan_scatter_kernel(ScatterArgs 
       a.adv_act[pos] = adv;
       a.old_act[pos] = old;
       if (a.gs_act) {
-        // dL/dlogp of -(1/N) min(rho A, clip(rho) A): the unclipped branch's
-        // derivative, or 0 where the clipped branch is the active minimum.
+        // dL/dlogp of -w (min(rho A, clip(rho) A) - beta KL), w = 1/N or the
+        // token's weight: the unclipped branch's derivative, or 0 where the
+        // clipped branch is the active minimum, plus w beta dKL/dlogp.
         const float lp = a.logp_in[t];
         const float rho = expf(lp - old);
         const bool cut = (adv > 0.0f && rho > 1.0f + a.eps_hi) || (adv < 0.0f && rho < 1.0f - a.eps_lo);
-        const float g = cut ? 0.0f : -(a.grad_loss / N) * adv * rho;
+        const float scale = a.token_weight ? a.grad_loss * a.token_weight[t] : a.grad_loss / N;
+        float g = cut ? 0.0f : -scale * adv * rho;
+        if (a.kl_beta != 0.0f) {
+          // k3: dKL/dl = 1 - exp(r - l) = -expm1(r - l); k1: 1
+          const float dkl = a.kl_est == 1 ? 1.0f : -expm1f(a.ref_logp[t] - lp);
+          g += scale * a.kl_beta * dkl;
+        }
         a.lse_act[pos] = a.lse_in[t];
         a.gs_act[pos] = g * a.inv_temp;
+      } else {
+        a.ref_act[pos] = a.ref_logp ? a.ref_logp[t] : 0.0f;
+        a.w_act[pos] = a.token_weight ? a.token_weight[t] : 0.0f;
       }
     }
     ++pos;
@@ -235,8 +251,13 @@ struct MergeArgs {
   const float* zy;
   const float* old_act;
   const float* adv_act;
+  const float* ref_act;
+  const float* w_act;
   const int32_t* idx;
   float eps_lo, eps_hi;
+  float kl_beta;
+  int32_t kl_est;
+  int32_t weighted;        // loss partials are w_n f_n (else f_n, divided by N at the end)
   float* logp_out;
   float* lse_out;
   double* blk_sum;
@@ -277,7 +298,13 @@ __global__ __launch_bounds__(256) void merge_loss_kernel(MergeArgs a) {
     const float A = a.adv_act[n];
     const float rho = expf(logp - a.old_act[n]);
     const float rc = fminf(fmaxf(rho, 1.0f - a.eps_lo), 1.0f + a.eps_hi);
-    sv = (double)fminf(rho * A, rc * A);
+    float f = fminf(rho * A, rc * A);
+    if (a.kl_beta != 0.0f) {
+      // k3: exp(u) - u - 1 = expm1(u) - u with u = r - l (no cancellation near u = 0)
+      const float u = a.ref_act[n] - logp;
+      f -= a.kl_beta * (a.kl_est == 1 ? -u : expm1f(u) - u);
+    }
+    sv = a.weighted ? (double)a.w_act[n] * (double)f : (double)f;
     hi = (A > 0.0f && rho > 1.0f + a.eps_hi);
     lo = (A < 0.0f && rho < 1.0f - a.eps_lo);
     const int t = a.idx[n];
@@ -299,7 +326,8 @@ __global__ __launch_bounds__(256) void merge_loss_kernel(MergeArgs a) {
 __global__ __launch_bounds__(256) void finalize_loss_kernel(int32_t nblk, const double* blk_sum,
                                                             const long long* blk_clip,
                                                             const int32_t* ctrl, int64_t n_norm,
-                                                            float* loss, int64_t* n_clip) {
+                                                            int32_t weighted, float* loss,
+                                                            int64_t* n_clip) {
   __shared__ double ssum[256];
   __shared__ long long shi[256], slo[256];
   double s = 0.0;
@@ -324,7 +352,7 @@ __global__ __launch_bounds__(256) void finalize_loss_kernel(int32_t nblk, const 
   if (threadIdx.x == 0) {
     const int n_act = ctrl[0];
     const double N = n_norm > 0 ? (double)n_norm : (double)n_act;
-    float L = N > 0 ? (float)(-ssum[0] / N) : 0.0f;
+    float L = weighted ? (float)(-ssum[0]) : (N > 0 ? (float)(-ssum[0] / N) : 0.0f);
     if (ctrl[1]) L = NAN;
     *loss = L;
     if (n_clip) {
@@ -367,7 +395,8 @@ int fail(int code, const char* msg) {
 struct Layout {
   int64_t T, A_pad, V_pad, Vc;
   int32_t d, V, esize, nblk, tiles_v, merge_blocks;
-  size_t ctrl, blk_cnt, blk_off, idx, y_act, adv_act, old_act, lse_act, gs_act, zy, blk_sum,
+  size_t ctrl, blk_cnt, blk_off, idx, y_act, adv_act, old_act, ref_act, w_act, lse_act, gs_act,
+      zy, blk_sum,
       blk_clip, H_act, part, Ht, Wt, G, Gt, fwd_total, total;
 };
 
@@ -408,6 +437,8 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   L->y_act = take(4 * A);
   L->adv_act = take(4 * A);
   L->old_act = take(4 * A);
+  L->ref_act = take(4 * A);
+  L->w_act = take(4 * A);
   L->lse_act = take(4 * A);
   L->gs_act = take(4 * A);
   L->zy = take(4 * A);
@@ -460,6 +491,10 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
     return bad(AGRL_E_FLAGS, "temperature must be finite and >= 0");
   if (o.dw_accumulate != 0 && o.dw_accumulate != 1) return bad(AGRL_E_FLAGS, "dw_accumulate must be 0 or 1");
   if (o.g_chunk_bytes < 0) return bad(AGRL_E_FLAGS, "g_chunk_bytes < 0");
+  if (!isfinite(o.kl_beta)) return bad(AGRL_E_FLAGS, "kl_beta must be finite");
+  if (o.kl_estimator != 0 && o.kl_estimator != 1) return bad(AGRL_E_FLAGS, "kl_estimator must be 0 or 1");
+  if (loss_inputs && o.kl_beta != 0.0f && T > 0 && !o.ref_logp)
+    return bad(AGRL_E_NULL, "kl_beta != 0 needs ref_logp");
   if (T > 0 && (!H || !token_id || !mask || (loss_inputs && (!adv || !old))))
     return bad(AGRL_E_NULL, "input pointer is NULL");
   if (!W) return bad(AGRL_E_NULL, "W is NULL");
@@ -562,6 +597,12 @@ int compact(const Common& c, const Layout& L, uint8_t* ws, const uint8_t* mask,
   a.gs_act = lse_in ? (float*)(ws + L.gs_act) : nullptr;
   a.logp_out = logp_out;
   a.lse_out = lse_out;
+  a.ref_logp = c.o.kl_beta != 0.0f ? c.o.ref_logp : nullptr;
+  a.token_weight = c.o.token_weight;
+  a.ref_act = (float*)(ws + L.ref_act);
+  a.w_act = (float*)(ws + L.w_act);
+  a.kl_beta = c.o.kl_beta;
+  a.kl_est = c.o.kl_estimator;
   a.eps_lo = c.eps_lo;
   a.eps_hi = c.eps_hi;
   a.grad_loss = grad_loss;
@@ -751,6 +792,11 @@ extern "C" int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32
   m.idx = (const int32_t*)(ws + L.idx);
   m.eps_lo = c.eps_lo;
   m.eps_hi = c.eps_hi;
+  m.ref_act = (const float*)(ws + L.ref_act);
+  m.w_act = (const float*)(ws + L.w_act);
+  m.kl_beta = c.o.kl_beta;
+  m.kl_est = c.o.kl_estimator;
+  m.weighted = c.o.token_weight != nullptr;
   m.logp_out = logp;
   m.lse_out = lse;
   m.blk_sum = (double*)(ws + L.blk_sum);
@@ -758,7 +804,8 @@ extern "C" int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32
   hipLaunchKernelGGL(merge_loss_kernel, dim3(L.merge_blocks), dim3(256), 0, s, m);
   hipLaunchKernelGGL(finalize_loss_kernel, dim3(1), dim3(256), 0, s, L.merge_blocks,
                      (const double*)(ws + L.blk_sum), (const long long*)(ws + L.blk_clip),
-                     (const int32_t*)(ws + L.ctrl), n_norm, loss, n_clip);
+                     (const int32_t*)(ws + L.ctrl), n_norm, (int32_t)(c.o.token_weight != nullptr),
+                     loss, n_clip);
   return hip_status(hipGetLastError());
 }
 
@@ -784,6 +831,8 @@ extern "C" int agrl_token_logprob(int64_t T, int64_t max_act, int32_t d, int32_t
   if (rc) return rc;
   if (T > 0 && (!logp || !lse)) return fail(AGRL_E_NULL, "agrl_token_logprob: output pointer is NULL");
   if (T == 0) return AGRL_OK;
+  c.o.kl_beta = 0.0f;          // loss-only options play no part here
+  c.o.token_weight = nullptr;
   hipStream_t s = (hipStream_t)stream;
   int* err = device_error_ptr();
   if (!err) return hip_status(hipErrorInvalidSymbol);
@@ -809,6 +858,11 @@ extern "C" int agrl_token_logprob(int64_t T, int64_t max_act, int32_t d, int32_t
   m.idx = (const int32_t*)(ws + L.idx);
   m.eps_lo = 0.0f;
   m.eps_hi = 0.0f;
+  m.ref_act = (const float*)(ws + L.ref_act);
+  m.w_act = (const float*)(ws + L.w_act);
+  m.kl_beta = 0.0f;
+  m.kl_est = 0;
+  m.weighted = 0;
   m.logp_out = logp;
   m.lse_out = lse;
   m.blk_sum = (double*)(ws + L.blk_sum);

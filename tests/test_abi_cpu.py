@@ -71,6 +71,12 @@ def test_forward_argument_errors(L):
     assert _fwd(L, opt=ctypes.byref(o)) == E_FLAGS
     o = agrl_options(dw_accumulate=2)
     assert _fwd(L, opt=ctypes.byref(o)) == E_FLAGS
+    o = agrl_options(kl_beta=0.1)                       # KL without a reference
+    assert _fwd(L, opt=ctypes.byref(o)) == E_NULL
+    o = agrl_options(kl_beta=float("inf"), ref_logp=1 << 12)
+    assert _fwd(L, opt=ctypes.byref(o)) == E_FLAGS
+    o = agrl_options(kl_beta=0.1, kl_estimator=2, ref_logp=1 << 12)
+    assert _fwd(L, opt=ctypes.byref(o)) == E_FLAGS
     # a workspace that is one byte short
     need = L.agrl_policy_loss_workspace_size(100, 0, 64, 50, 0, None)
     assert _fwd(L, ws=1 << 12, wsb=need - 1) == E_WS
@@ -123,6 +129,10 @@ def test_adv_norm_argument_errors(L):
     assert f(10, 1, 1, 0, p, p, p, None, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
     o = agrl_options(std_eps=-1.0)
     assert f(10, 1, 1, 0, p, p, p, None, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
+    o = agrl_options(drop_uniform_groups=1)            # dynamic sampling needs groups
+    assert f(10, 1, 1, 0, p, p, p, None, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
+    o = agrl_options(drop_uniform_groups=2)
+    assert f(10, 1, 1, 1, p, p, p, p, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
 
 
 def test_workspace_size(L):

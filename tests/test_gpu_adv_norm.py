@@ -16,13 +16,13 @@ pytestmark = pytest.mark.gpu
 KEYS = ("act_count", "task_count", "task_mean", "task_std", "adv_traj", "adv_tok")
 
 
-def _gpu(traj_id, mask, traj_task, traj_group, reward, n_task, n_group, ddof=0):
+def _gpu(traj_id, mask, traj_task, traj_group, reward, n_task, n_group, ddof=0, drop=False):
     import paper_2510_04206_amd as P
     dev = "cuda"
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     out = P.task_adv_norm(t(traj_id), t(mask), t(traj_task),
                           None if traj_group is None else t(traj_group), t(reward), n_task,
-                          n_group, opt={"std_ddof": ddof})
+                          n_group, opt={"std_ddof": ddof, "drop_uniform_groups": int(drop)})
     assert P.agrl_get_device_error() == 0
     return {k: v.cpu().numpy() for k, v in out.items()}
 
@@ -59,8 +59,26 @@ def test_adv_norm_golden_cases(case):
     args = (np.array(case["traj_id"], np.int32), np.array(case["mask"], np.uint8),
             np.array(case["traj_task"], np.int32), tg, np.array(case["reward"], np.float32),
             case["n_task"], case["n_group"])
-    r = oracle.task_adv_norm(*args, ddof=case["ddof"])
-    g = _gpu(*args, ddof=case["ddof"])
+    drop = case.get("drop_uniform", False)
+    r = oracle.task_adv_norm(*args, ddof=case["ddof"], drop_uniform=drop)
+    g = _gpu(*args, ddof=case["ddof"], drop=drop)
+    _assert_bitwise(g, r)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 5])
+@pytest.mark.parametrize("ddof", [0, 1])
+def test_adv_norm_drop_uniform_groups_bit_exact(k, ddof):
+    """DAPO dynamic sampling with planted all-equal groups (workload 5 also has
+    whole tasks of equal rewards)."""
+    w = gen.config(k, tensors=False)
+    R = w.reward.copy()
+    rng = np.random.default_rng(100 + k)
+    for g in rng.choice(w.n_group, size=max(1, w.n_group // 4), replace=False):
+        R[w.traj_group == g] = R[w.traj_group == g][0]
+    log(f"adv_norm drop_uniform workload {k} ddof={ddof}")
+    args = (w.g_traj_id, w.g_mask, w.traj_task, w.traj_group, R, w.n_task, w.n_group)
+    r = oracle.task_adv_norm(*args, ddof=ddof, drop_uniform=True)
+    g = _gpu(*args, ddof=ddof, drop=True)
     _assert_bitwise(g, r)
 
 
