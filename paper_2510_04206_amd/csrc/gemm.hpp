@@ -64,7 +64,22 @@ struct GemmShape {
   int32_t K;               // multiple of BK (used when k_dev == nullptr)
   const int32_t* k_dev;    // K read on the device, rounded up to BK
   int32_t group_m;         // row-tiles per tile-order group
+  // bf16 kernel only: the operand is stored stage-tiled (see tiled_index) and
+  // lda / ldb is its padded K extent, a multiple of 64
+  int32_t a_tiled, b_tiled;
 };
+
+// Stage-tiled bf16 layout of a matrix with rows r and K-columns k (K padded to
+// k_pad, a multiple of 64; rows padded to a multiple of 256): the 256 x 64
+// block (r / 256, k / 64) is 32 KiB contiguous, row-major with 128-byte rows,
+// and 16-byte chunk c of a block row rr sits at chunk c ^ ((rr >> 1) & 7), the
+// LDS swizzle of the kernel below.  One K stage of a 256-row tile is then one
+// contiguous 32 KiB block that copies into LDS unchanged (every copy moves
+// 1 KiB of consecutive bytes), and a stage's rows share DRAM pages.
+__host__ __device__ __forceinline__ int64_t tiled_index(int64_t r, int64_t k, int64_t k_pad) {
+  return (((r >> 8) * (k_pad >> 6) + (k >> 6)) << 14) + ((r & 255) << 6) +
+         ((((k & 63) >> 3) ^ ((r >> 1) & 7)) << 3) + (k & 7);
+}
 
 // Accumulator element (i, j, r) of a wave sits at
 //   row = wm*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4,  col = wn*128 + j*32 + lane%32.
@@ -411,29 +426,36 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     grouped_tile(L, p ? tmp[1] : tmp[0], p ? tnp[1] : tnp[0], g.group_m, tm, tn);
     const int64_t lda_b = g.lda * 2, ldb_b = g.ldb * 2;
     const int m0 = tm * GBM, n0 = tn * GBN;
-    const uint8_t* a_base = (const uint8_t*)g.A + (int64_t)m0 * lda_b;
-    const uint8_t* b_base = (const uint8_t*)g.B + (int64_t)n0 * ldb_b;
+    // row-major: a tile starts at its first row and a stage advances 128 bytes;
+    // stage-tiled: a tile starts at its first 32 KiB block and a stage advances one
+    const uint8_t* a_base = (const uint8_t*)g.A + (g.a_tiled ? (int64_t)tm * (g.lda >> 6) * STAGE / 2
+                                                             : (int64_t)m0 * lda_b);
+    const uint8_t* b_base = (const uint8_t*)g.B + (g.b_tiled ? (int64_t)tn * (g.ldb >> 6) * STAGE / 2
+                                                             : (int64_t)n0 * ldb_b);
+    const int64_t a_ks = g.a_tiled ? STAGE / 2 : ROW, b_ks = g.b_tiled ? STAGE / 2 : ROW;
     // copy q < 8 moves A rows [64 wave + 8 q, +8), q >= 8 the same rows of B;
-    // lane i fetches chunk (i & 7) ^ swizzle(row) of row i / 8 (clamped to the
-    // last valid row; those products are discarded by the epilogue)
+    // lane i fetches chunk (i & 7) ^ swizzle(row) of row i / 8 (row-major: clamped
+    // to the last valid row, those products are discarded by the epilogue;
+    // stage-tiled: the chunk is already in place, the copy is 1 KiB contiguous)
     uint32_t offa[IPW], offb[IPW];
 #pragma unroll
     for (int b = 0; b < IPW; ++b) {
       const int row = wave * 64 + b * RPI + (lane >> 3);
       const int ch = ((lane & 7) ^ row_swizzle(row)) << 4;
-      offa[b] = (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
-      offb[b] = (uint32_t)(min(row, g.N - 1 - n0) * ldb_b + ch);
+      offa[b] = g.a_tiled ? (uint32_t)(row * ROW + (lane & 7) * 16)
+                          : (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
+      offb[b] = g.b_tiled ? (uint32_t)(row * ROW + (lane & 7) * 16)
+                          : (uint32_t)(min(row, g.N - 1 - n0) * ldb_b + ch);
     }
 
     auto copy = [&](int s, int q) {
       const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE);
-      const int64_t kb = (int64_t)s * ROW;
       const int b = q % IPW;
       const uint32_t r0 = (uint32_t)(wave * 64 + b * RPI) * ROW;
       if (q < IPW)
-        copy16(a_base + kb + offa[b], __builtin_amdgcn_readfirstlane(st + r0));
+        copy16(a_base + s * a_ks + offa[b], __builtin_amdgcn_readfirstlane(st + r0));
       else
-        copy16(b_base + kb + offb[b], __builtin_amdgcn_readfirstlane(st + GBM * ROW + r0));
+        copy16(b_base + s * b_ks + offb[b], __builtin_amdgcn_readfirstlane(st + GBM * ROW + r0));
     };
 
     f32x16 acc[4][4];
@@ -696,6 +718,7 @@ struct LogitGradArgs {
   int64_t ldgt;
   float scale;
   int32_t col0;          // vocabulary index of this chunk's column 0
+  int32_t tiled;         // bf16: G and G^T are written stage-tiled (ldg, ldgt = padded K)
 };
 
 template <typename T>
@@ -829,7 +852,9 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
         const int row = q >> 5, c16 = q & 31;
         const int trow = 64 * h + (row < 64 ? row : row + 64);
         const u32x4 v = *(const u32x4*)(smem + EPI_GS + row * EPI_G_ROW + c16 * 16);
-        *(u32x4*)(G + (int64_t)(m0 + trow) * ldg + n0 + c16 * 8) = v;
+        const int64_t at = tiled ? tiled_index(m0 + trow, n0 + c16 * 8, ldg)
+                                 : (int64_t)(m0 + trow) * ldg + n0 + c16 * 8;
+        *(u32x4*)(G + at) = v;
       }
       // Gt: 256 rows (tile columns) of 16 chunks of 8 tile rows each
 #pragma unroll 4
@@ -840,7 +865,9 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
         u32x4 v = *(const u32x4*)(smem + EPI_GTS + row * 256 + (((2 * c16) ^ x) >> 1) * 16);
         if (x & 1) v = u32x4{v.z, v.w, v.x, v.y};
         const int trow = 64 * h + (c16 < 8 ? 8 * c16 : 8 * c16 + 64);
-        *(u32x4*)(Gt + (int64_t)(n0 + row) * ldgt + m0 + trow) = v;
+        const int64_t at = tiled ? tiled_index(n0 + row, m0 + trow, ldgt)
+                                 : (int64_t)(n0 + row) * ldgt + m0 + trow;
+        *(u32x4*)(Gt + at) = v;
       }
     }
   }

@@ -213,12 +213,13 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint8_t* __restr
 
 // dst[c][r] = src[r][c]; rows in [n_rows, n_rows_pad) are written as 0.
 // n_rows comes from ctrl[0] (rounded up to 256 for the padded extent) when
-// rows_from_ctrl is set.  64 x 64 element tiles through LDS.
+// ctrl is given.  64 x 64 element tiles through LDS.  With `tiled`, dst is
+// stage-tiled (tiled_index, K = r padded to ld_dst) instead of row-major.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ src, int64_t ld_src,
                                                         T* dst, int64_t ld_dst, int64_t n_rows,
                                                         int64_t n_rows_pad, int64_t n_cols,
-                                                        const int32_t* ctrl) {
+                                                        const int32_t* ctrl, int32_t tiled) {
   __shared__ T tile[64][65];
   if (ctrl) {
     n_rows = ctrl[0];
@@ -238,7 +239,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ sr
   for (int k = 0; k < 16; ++k) {
     const int cc = ty + 4 * k;
     const int64_t c = c0 + cc, r = r0 + tx;
-    if (c < n_cols && r < n_rows_pad) dst[c * ld_dst + r] = tile[tx][cc];
+    if (c < n_cols && r < n_rows_pad)
+      dst[tiled ? tiled_index(c, r, ld_dst) : c * ld_dst + r] = tile[tx][cc];
   }
 }
 
@@ -451,8 +453,10 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   const size_t fwd_end = off;
   L->fwd_total = fwd_end;
   off = shared_at;
-  L->Ht = take((size_t)d * A * L->esize);
-  L->Wt = take((size_t)d * L->V_pad * L->esize);
+  // H^T and W^T: d rows padded to a whole 256-row tile (bf16 stage-tiled layout)
+  const size_t d_pad = (size_t)round_up(d, kRowPad);
+  L->Ht = take(d_pad * A * L->esize);
+  L->Wt = take(d_pad * L->V_pad * L->esize);
   L->G = take(A * (size_t)L->Vc * L->esize);
   L->Gt = take((size_t)L->Vc * A * L->esize);
   if (fwd_end > off) off = fwd_end;
@@ -657,13 +661,16 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
   T* Wt = (T*)(ws + L.Wt);
   T* G = (T*)(ws + L.G);
   T* Gt = (T*)(ws + L.Gt);
-  // H_act^T [d][A_pad] (zero beyond the action rows) and W^T [d][V_pad] (zero beyond V)
+  // H_act^T [d][A_pad] (zero beyond the action rows) and W^T [d][V_pad] (zero
+  // beyond V); for bf16 both, and G and G^T, are stage-tiled: every stage of the
+  // two products below is a contiguous 32 KiB block per operand tile
+  constexpr int32_t tiled = std::is_same<T, __bf16>::value ? 1 : 0;
   hipLaunchKernelGGL((transpose_kernel<S>), dim3((unsigned)(L.A_pad / 64), (unsigned)cdiv(c.d, 64)),
                      dim3(256), 0, s, (const S*)(ws + L.H_act), (int64_t)c.d, (S*)Ht, L.A_pad,
-                     (int64_t)0, (int64_t)0, (int64_t)c.d, ctrl);
+                     (int64_t)0, (int64_t)0, (int64_t)c.d, ctrl, tiled);
   hipLaunchKernelGGL((transpose_kernel<S>), dim3((unsigned)(L.V_pad / 64), (unsigned)cdiv(c.d, 64)),
                      dim3(256), 0, s, (const S*)W, (int64_t)c.d, (S*)Wt, L.V_pad, (int64_t)c.V,
-                     L.V_pad, (int64_t)c.d, (const int32_t*)nullptr);
+                     L.V_pad, (int64_t)c.d, (const int32_t*)nullptr, tiled);
   const int row_tiles = (int)(L.A_pad / GBM);
   const int d_tiles = cdiv(c.d, GBN);
   for (int64_t v0 = 0; v0 < c.V; v0 += L.Vc) {
@@ -689,6 +696,7 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       e.ldgt = L.A_pad;
       e.scale = c.inv_temp;
       e.col0 = (int32_t)v0;
+      e.tiled = tiled;
       launch_gemm<T>(&g, &e, 1, row_tiles * nv_tiles, (int32_t*)(ws + L.ctrl + 64), c.o,
                      PH_RECOMPUTE, -1, s);
     }
@@ -698,8 +706,11 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       GemmShape g[2] = {};
       g[0].A = G;
       g[0].lda = L.Vc;
-      g[0].B = Wt + v0;
+      // the chunk's first vocabulary column: a row offset, or whole 64-column blocks
+      g[0].B = tiled ? (const void*)(Wt + v0 * 256) : (const void*)(Wt + v0);
       g[0].ldb = L.V_pad;
+      g[0].a_tiled = tiled;
+      g[0].b_tiled = tiled;
       g[0].m_dev = ctrl;
       g[0].N = c.d;
       g[0].K = (int32_t)round_up(nv, KStage<T>::BK);
@@ -708,6 +719,8 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       g[1].lda = L.A_pad;
       g[1].B = Ht;
       g[1].ldb = L.A_pad;
+      g[1].a_tiled = tiled;
+      g[1].b_tiled = tiled;
       g[1].M = nv;
       g[1].N = c.d;
       g[1].k_dev = ctrl;
