@@ -244,6 +244,48 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ sr
   }
 }
 
+// bf16 (2-byte) variant of transpose_kernel with 16-byte global accesses: each
+// 64 x 64 tile is read as 8-element row chunks, written to LDS transposed
+// (66-element rows: the 16-bit stores of a wave hit distinct banks), and read
+// back as 8-element chunks of the output rows.  Same arguments and padding
+// rules; d (the source row length) is a multiple of 64.
+__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t* __restrict__ src,
+                                                          int64_t ld_src, uint16_t* dst,
+                                                          int64_t ld_dst, int64_t n_rows,
+                                                          int64_t n_rows_pad, int64_t n_cols,
+                                                          const int32_t* ctrl, int32_t tiled) {
+  constexpr int P = 66;
+  __shared__ uint16_t tile_t[64 * P];
+  if (ctrl) {
+    n_rows = ctrl[0];
+    n_rows_pad = round_up(n_rows, kRowPad);
+  }
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  if (r0 >= n_rows_pad) return;
+  for (int k = 0; k < 2; ++k) {
+    const int id = threadIdx.x + 256 * k;
+    const int rr = id >> 3, c8 = id & 7;
+    const int64_t r = r0 + rr;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < n_rows) v = *(const u32x4*)(src + r * ld_src + c0 + 8 * c8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tile_t[(8 * c8 + 2 * e) * P + rr] = (uint16_t)v[e];
+      tile_t[(8 * c8 + 2 * e + 1) * P + rr] = (uint16_t)(v[e] >> 16);
+    }
+  }
+  __syncthreads();
+  for (int k = 0; k < 2; ++k) {
+    const int id = threadIdx.x + 256 * k;
+    const int c = id >> 3, r8 = id & 7;
+    const uint32_t* t32 = (const uint32_t*)(tile_t + c * P + 8 * r8);   // 4-byte aligned
+    const u32x4 v = {t32[0], t32[1], t32[2], t32[3]};
+    const int64_t oc = c0 + c, orr = r0 + 8 * r8;
+    if (oc < n_cols && orr < n_rows_pad)
+      *(u32x4*)(dst + (tiled ? tiled_index(oc, orr, ld_dst) : oc * ld_dst + orr)) = v;
+  }
+}
+
 // ------------------------------------------------------------------ forward epilogue
 struct MergeArgs {
   const int32_t* ctrl;
@@ -665,12 +707,23 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
   // beyond V); for bf16 both, and G and G^T, are stage-tiled: every stage of the
   // two products below is a contiguous 32 KiB block per operand tile
   constexpr int32_t tiled = std::is_same<T, __bf16>::value ? 1 : 0;
-  hipLaunchKernelGGL((transpose_kernel<S>), dim3((unsigned)(L.A_pad / 64), (unsigned)cdiv(c.d, 64)),
-                     dim3(256), 0, s, (const S*)(ws + L.H_act), (int64_t)c.d, (S*)Ht, L.A_pad,
-                     (int64_t)0, (int64_t)0, (int64_t)c.d, ctrl, tiled);
-  hipLaunchKernelGGL((transpose_kernel<S>), dim3((unsigned)(L.V_pad / 64), (unsigned)cdiv(c.d, 64)),
-                     dim3(256), 0, s, (const S*)W, (int64_t)c.d, (S*)Wt, L.V_pad, (int64_t)c.V,
-                     L.V_pad, (int64_t)c.d, (const int32_t*)nullptr, tiled);
+  const dim3 gh((unsigned)(L.A_pad / 64), (unsigned)cdiv(c.d, 64));
+  const dim3 gw((unsigned)(L.V_pad / 64), (unsigned)cdiv(c.d, 64));
+  if constexpr (sizeof(S) == 2) {
+    hipLaunchKernelGGL(transpose16_kernel, gh, dim3(256), 0, s, (const uint16_t*)(ws + L.H_act),
+                       (int64_t)c.d, (uint16_t*)Ht, L.A_pad, (int64_t)0, (int64_t)0,
+                       (int64_t)c.d, ctrl, tiled);
+    hipLaunchKernelGGL(transpose16_kernel, gw, dim3(256), 0, s, (const uint16_t*)W, (int64_t)c.d,
+                       (uint16_t*)Wt, L.V_pad, (int64_t)c.V, L.V_pad, (int64_t)c.d,
+                       (const int32_t*)nullptr, tiled);
+  } else {
+    hipLaunchKernelGGL((transpose_kernel<S>), gh, dim3(256), 0, s, (const S*)(ws + L.H_act),
+                       (int64_t)c.d, (S*)Ht, L.A_pad, (int64_t)0, (int64_t)0, (int64_t)c.d, ctrl,
+                       tiled);
+    hipLaunchKernelGGL((transpose_kernel<S>), gw, dim3(256), 0, s, (const S*)W, (int64_t)c.d,
+                       (S*)Wt, L.V_pad, (int64_t)c.V, L.V_pad, (int64_t)c.d,
+                       (const int32_t*)nullptr, tiled);
+  }
   const int row_tiles = (int)(L.A_pad / GBM);
   const int d_tiles = cdiv(c.d, GBN);
   for (int64_t v0 = 0; v0 < c.V; v0 += L.Vc) {
