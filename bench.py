@@ -253,7 +253,7 @@ def main():
     per_step = [phase_ms[0], phase_ms[1] * n_chunks, phase_ms[2] * n_chunks, phase_ms[3] * n_chunks]
     dom = int(np.argmax(per_step))
     achieved = per_launch[dom] / (phase_ms[dom] * 1e-3)
-    kernel_names = ["gemm_bf16_kernel<EpiLsePartial>", "gemm_bf16_kernel<EpiLogitGrad>",
+    kernel_names = ["gemm_bf16_kernel<EpiLseCols>", "gemm_bf16_kernel<EpiLogitGrad>",
                     "gemm_bf16_kernel<EpiStore>", "gemm_bf16_kernel<EpiStore>"]
     if code != P.AGRL_BF16:
         kernel_names = [k.replace("gemm_bf16_kernel", "gemm_nt_kernel") for k in kernel_names]

@@ -60,7 +60,8 @@ struct GemmShape {
   int64_t ldb;
   int32_t M;               // rows of A (used when m_dev == nullptr)
   const int32_t* m_dev;    // rows of A read on the device
-  int32_t N;               // rows of B
+  int32_t N;               // rows of B (used when n_dev == nullptr)
+  const int32_t* n_dev;    // rows of B read on the device
   int32_t K;               // multiple of BK (used when k_dev == nullptr)
   const int32_t* k_dev;    // K read on the device, rounded up to BK
   int32_t group_m;         // row-tiles per tile-order group
@@ -222,9 +223,10 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int M = g.m_dev ? *g.m_dev : g.M;
+  const int N = g.n_dev ? *g.n_dev : g.N;
   const int K = g.k_dev ? cdiv(*g.k_dev, BK) * BK : g.K;
-  if (M <= 0 || g.N <= 0) return;
-  const int tiles_m = cdiv(M, GBM), tiles_n = cdiv(g.N, GBN);
+  if (M <= 0 || N <= 0) return;
+  const int tiles_m = cdiv(M, GBM), tiles_n = cdiv(N, GBN);
   const int total = tiles_m * tiles_n;
   const int nk = K / BK;
   const uint8_t* A = (const uint8_t*)g.A;
@@ -244,20 +246,20 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     if (nk > 0) {
-      dma_stage(smem, A, lda_b, m0, M, B, ldb_b, n0, g.N, 0, wave, lane);
+      dma_stage(smem, A, lda_b, m0, M, B, ldb_b, n0, N, 0, wave, lane);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       for (int kt = 0; kt < nk; ++kt) {
         const uint8_t* cur = smem + (kt & 1) * STAGE_BYTES;
         if (kt + 1 < nk)
-          dma_stage(smem + ((kt + 1) & 1) * STAGE_BYTES, A, lda_b, m0, M, B, ldb_b, n0, g.N,
+          dma_stage(smem + ((kt + 1) & 1) * STAGE_BYTES, A, lda_b, m0, M, B, ldb_b, n0, N,
                     (int64_t)(kt + 1) * BK * (int64_t)sizeof(T), wave, lane);
         compute_stage<T>(cur, acc, wm, wn, lane);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
       }
     }
-    epi(acc, m0, n0, tn, M, g.N, smem, wm, wn, lane, tid);
+    epi(acc, m0, n0, tn, M, N, smem, wm, wn, lane, tid);
     __syncthreads();
   }
 }
@@ -382,17 +384,18 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   const int wm = wave >> 1, wn = wave & 1;
   const int nq = min(8, (int)gridDim.x);
   const int qi = blockIdx.x % nq;
-  int Mp[2], Kp[2], tmp[2], tnp[2];
+  int Mp[2], Np[2], Kp[2], tmp[2], tnp[2];
   QueueShare sh[2];
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const GemmShape& gp = bat.g[p];
     // device-read sizes are the same in every lane; keep them scalar (see below)
     Mp[p] = __builtin_amdgcn_readfirstlane(gp.m_dev ? *gp.m_dev : gp.M);
+    Np[p] = __builtin_amdgcn_readfirstlane(gp.n_dev ? *gp.n_dev : gp.N);
     Kp[p] = __builtin_amdgcn_readfirstlane(gp.k_dev ? cdiv(*gp.k_dev, SK) * SK : gp.K);
     tmp[p] = cdiv(Mp[p], GBM);
-    tnp[p] = cdiv(gp.N, GBN);
-    const int total = (p < bat.n && Mp[p] > 0 && gp.N > 0) ? tmp[p] * tnp[p] : 0;
+    tnp[p] = cdiv(Np[p], GBN);
+    const int total = (p < bat.n && Mp[p] > 0 && Np[p] > 0) ? tmp[p] * tnp[p] : 0;
     sh[p] = queue_share(total, qi, nq);
   }
 
@@ -420,6 +423,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     const GemmShape g = p ? bat.g[1] : bat.g[0];
     const Epi epi = p ? bat.e[1] : bat.e[0];
     const int M = p ? Mp[1] : Mp[0];
+    const int N = p ? Np[1] : Np[0];
     const int nk = (p ? Kp[1] : Kp[0]) / SK;
     int tm, tn;
     const int L = p ? queue_tile(t - sh[0].len, sh[1], qi, nq) : queue_tile(t, sh[0], qi, nq);
@@ -445,7 +449,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       offa[b] = g.a_tiled ? (uint32_t)(row * ROW + (lane & 7) * 16)
                           : (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
       offb[b] = g.b_tiled ? (uint32_t)(row * ROW + (lane & 7) * 16)
-                          : (uint32_t)(min(row, g.N - 1 - n0) * ldb_b + ch);
+                          : (uint32_t)(min(row, N - 1 - n0) * ldb_b + ch);
     }
 
     auto copy = [&](int s, int q) {
@@ -537,7 +541,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __syncthreads();
-    epi(acc, m0, n0, tn, M, g.N, smem, wm, wn, lane, tid);
+    epi(acc, m0, n0, tn, M, N, smem, wm, wn, lane, tid);
     __syncthreads();
   }
 }
@@ -689,6 +693,102 @@ struct EpiLsePartial {
       const float s = (a.y > 0.0f ? a.y * __expf(a.x - m) : 0.0f) +
                       (b.y > 0.0f ? b.y * __expf(b.x - m) : 0.0f);
       part[(int64_t)tn * ld_part + row] = f32x2{m, s};
+    }
+  }
+};
+
+// Forward partial log-sum-exp on a transposed tile: rows are vocabulary
+// entries (A = W), columns are compacted tokens (B = H_act).  The accumulator
+// layout gives every lane 64 rows of each of its 4 token columns, so the
+// reduction over the tile's vocabulary is lane-local except for one exchange
+// between lanes l and l ^ 32 (the two 4-row halves) and one merge of the two
+// row waves through LDS.  Same outputs as EpiLsePartial: (max, sum exp) per
+// token and vocabulary tile, and the target logit.
+struct EpiLseCols {
+  const int32_t* y;      // [tokens] target id of each compacted row
+  f32x2* part;           // [tiles_v][ld_part] (max, sum exp) per token and vocabulary tile
+  int64_t ld_part;
+  float* zy;             // [tokens] logit of the target token
+  float scale;           // 1 / temperature
+
+  template <bool FULL>
+  __device__ __forceinline__ void cols(const f32x16 (&acc)[4][4], int m0, int n0, int M,
+                                       const int* sy, f32x2* red, int wm, int wn,
+                                       int lane) const {
+    const float k1 = scale * 1.44269504088896341f;
+    // this lane's rows are wm * 128 + hb + o with o = 32 i + 8 (r >> 2) + (r & 3)
+    const int hb = 4 * (lane >> 5);
+    const int lim = M - m0 - wm * 128 - hb;     // rows o >= lim are beyond the vocabulary
+    auto live = [&](int i, int r) { return FULL || 32 * i + 8 * (r >> 2) + (r & 3) < lim; };
+    float mx[4], sm[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mx[j] = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mx[j] = fmaxf(mx[j], live(i, r) ? acc[i][j][r] : -INFINITY);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      mx[j] = fmaxf(mx[j], __shfl_xor(mx[j], 32));
+      sm[j] = 0.0f;
+    }
+    float mk[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mk[j] = FULL || mx[j] != -INFINITY ? -mx[j] * k1 : 0.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], k1, mk[j]));
+          sm[j] += live(i, r) ? e : 0.0f;
+        }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sm[j] += __shfl_xor(sm[j], 32);
+      const int c = wn * 128 + j * 32 + (lane & 31);
+      if (lane < 32) red[wm * GBN + c] = f32x2{mx[j] * scale, sm[j]};
+      // target logit: local row o of the target, held here iff 0 <= o < 128 and
+      // bit 2 of o is clear; the register is picked by a select tree over o's bits
+      const int o = sy[c] - wm * 128 - hb;
+      float v[64];
+#pragma unroll
+      for (int q = 0; q < 64; ++q) v[q] = acc[q >> 4][j][q & 15];
+      const int idx = ((o >> 5) << 4) | (((o >> 3) & 3) << 2) | (o & 3);
+#pragma unroll
+      for (int b = 0, w = 32; b < 6; ++b, w >>= 1) {
+        const bool hi = (idx >> b) & 1;
+#pragma unroll
+        for (int q = 0; q < w; ++q) v[q] = hi ? v[2 * q + 1] : v[2 * q];
+      }
+      if ((unsigned)o < 128u && (o & 4) == 0) zy[n0 + c] = v[0] * scale;
+    }
+  }
+
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                             int N, uint8_t* smem, int wm, int wn, int lane,
+                                             int tid) const {
+    int* sy = (int*)smem;
+    f32x2* red = (f32x2*)(smem + 1024);
+    // target row relative to the tile (-1: dead column; a target outside the
+    // tile matches no row)
+    sy[tid] = (n0 + tid < N) ? y[n0 + tid] - m0 : -1;
+    __syncthreads();
+    if (m0 + GBM <= M)
+      cols<true>(acc, m0, n0, M, sy, red, wm, wn, lane);
+    else
+      cols<false>(acc, m0, n0, M, sy, red, wm, wn, lane);
+    __syncthreads();
+    const int col = n0 + tid;
+    if (col < N) {
+      const f32x2 a = red[tid], b = red[GBN + tid];
+      const float m = fmaxf(a.x, b.x);
+      const float s = (a.y > 0.0f ? a.y * __expf(a.x - m) : 0.0f) +
+                      (b.y > 0.0f ? b.y * __expf(b.x - m) : 0.0f);
+      part[(int64_t)(m0 / GBM) * ld_part + col] = f32x2{m, s};
     }
   }
 };

@@ -666,23 +666,43 @@ int compact(const Common& c, const Layout& L, uint8_t* ws, const uint8_t* mask,
 
 template <typename T>
 void fwd_gemm(const Common& c, const Layout& L, uint8_t* ws, const void* W, hipStream_t s) {
+  const int32_t* n_act = (const int32_t*)(ws + L.ctrl);
+  const int max_tiles = (int)(L.A_pad / GBM) * L.tiles_v;
   GemmShape g = {};
-  g.A = ws + L.H_act;
-  g.lda = c.d;
-  g.B = W;
-  g.ldb = c.d;
-  g.m_dev = (const int32_t*)(ws + L.ctrl);
-  g.N = c.V;
   g.K = c.d;
   g.group_m = 8;
-  EpiLsePartial e;
-  e.y = (const int32_t*)(ws + L.y_act);
-  e.part = (f32x2*)(ws + L.part);
-  e.ld_part = L.A_pad;
-  e.zy = (float*)(ws + L.zy);
-  e.scale = c.inv_temp;
-  const int max_tiles = (int)(L.A_pad / GBM) * L.tiles_v;
-  launch_gemm<T>(&g, &e, 1, max_tiles, (int32_t*)(ws + L.ctrl + 64), c.o, PH_FWD, -1, s);
+  if constexpr (std::is_same<T, __bf16>::value) {
+    // transposed tile (rows: vocabulary, columns: action tokens), so that the
+    // log-sum-exp over the vocabulary reduces mostly inside each lane
+    g.A = W;
+    g.lda = c.d;
+    g.M = c.V;
+    g.B = ws + L.H_act;
+    g.ldb = c.d;
+    g.N = (int32_t)L.A_pad;
+    g.n_dev = n_act;
+    EpiLseCols e;
+    e.y = (const int32_t*)(ws + L.y_act);
+    e.part = (f32x2*)(ws + L.part);
+    e.ld_part = L.A_pad;
+    e.zy = (float*)(ws + L.zy);
+    e.scale = c.inv_temp;
+    launch_gemm<T>(&g, &e, 1, max_tiles, (int32_t*)(ws + L.ctrl + 64), c.o, PH_FWD, -1, s);
+  } else {
+    g.A = ws + L.H_act;
+    g.lda = c.d;
+    g.B = W;
+    g.ldb = c.d;
+    g.m_dev = n_act;
+    g.N = c.V;
+    EpiLsePartial e;
+    e.y = (const int32_t*)(ws + L.y_act);
+    e.part = (f32x2*)(ws + L.part);
+    e.ld_part = L.A_pad;
+    e.zy = (float*)(ws + L.zy);
+    e.scale = c.inv_temp;
+    launch_gemm<T>(&g, &e, 1, max_tiles, (int32_t*)(ws + L.ctrl + 64), c.o, PH_FWD, -1, s);
+  }
 }
 
 template <typename T>
