@@ -70,6 +70,59 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+class ClockSampler:
+    """Samples the shader clock the driver reports (the starred line of
+    pp_dpm_sclk in sysfs) from a background thread while the steps run: the
+    sustained clock under this load, against which the published peak (quoted
+    at 2.4 GHz) is rescaled.  Reports None where the file is not readable."""
+
+    def __init__(self, period_s: float = 0.01):
+        import glob
+        import threading
+        files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = files[0] if files else None
+        self.period = period_s
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        import re
+        try:
+            with open(self.path) as f:
+                for line in f:
+                    m = re.search(r"(\d+)\s*Mhz\s*\*", line)
+                    if m:
+                        return int(m.group(1))
+        except OSError:
+            return None
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.path:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self.path:
+            self._stop.set()
+            self._thread.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        a = np.array(self.samples, dtype=np.float64)
+        return {"mean": float(a.mean()), "min": float(a.min()), "max": float(a.max()),
+                "samples": int(a.size), "source": self.path}
+
+
 def kernel_sources_digest() -> str:
     """sha256 over the HIP sources and the build script (counters go stale when these change)."""
     h = hashlib.sha256()
@@ -206,11 +259,13 @@ def main():
     log(f"warm-up done; loss {pl.loss.item():.6g}")
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    start.record()
-    for i in range(Wm, Wm + K):
-        step(i)
-    end.record()
-    torch.cuda.synchronize()
+    with ClockSampler() as clock:
+        start.record()
+        for i in range(Wm, Wm + K):
+            step(i)
+        end.record()
+        torch.cuda.synchronize()
+    sclk = clock.summary()
     total_ms = start.elapsed_time(end)
     ms = total_ms / K
     if P.agrl_get_device_error() != 0:
@@ -302,7 +357,14 @@ def main():
                      "traffic_unit": "bytes per launch (HBM reads + writes, rocprofv3 FETCH_SIZE "
                                      "and WRITE_SIZE scaled by a copy kernel of known size)",
                      "flops_per_launch": per_launch[dom]},
+        "sclk_mhz": sclk,
     }
+    if sclk:
+        # the published peak is quoted at 2.4 GHz: the same fractions at the
+        # shader clock sampled during the timed steps
+        at_clock = peak * sclk["mean"] / 2400.0
+        out["mfma_frac_at_sampled_clock"] = step_flops / (ms * 1e-3) / at_clock
+        out["roofline"]["frac_at_sampled_clock"] = achieved / at_clock
     if args.cpu_tokens > 0:
         adv_host = adv_tok[:T].cpu().numpy()
         log(f"timing the oracle on {args.cpu_tokens} action tokens ...")
