@@ -95,6 +95,24 @@ def task_adv_norm(traj_id, mask, traj_task, traj_group, reward, n_task, n_group=
     return out
 
 
+def sequence_mean_weights(traj_id, mask, n_traj):
+    """Per-token weights of the sequence-level aggregation (App. B.2, GRPO's mean
+    over responses of per-response token means) for one micro-batch: returns
+    (count [n_traj] int32, weights [T] fp32)."""
+    lib = _load()
+    traj_id = np.ascontiguousarray(traj_id, np.int32)
+    mask = np.ascontiguousarray(mask, np.uint8)
+    T = traj_id.shape[0]
+    count = np.zeros(n_traj, np.int32)
+    w = np.zeros(T, np.float32)
+    f = lib.oracle_sequence_mean_weights
+    f.restype = ctypes.c_int
+    rc = f(ctypes.c_int64(T), ctypes.c_int32(n_traj), _p(traj_id), _p(mask), _p(count), _p(w))
+    if rc != 0:
+        raise ValueError("oracle_sequence_mean_weights: trajectory id out of range")
+    return count, w
+
+
 def policy_loss(H, W, token_id, mask, adv, old_logp, eps_lo=0.2, eps_hi=0.2, n_norm=0,
                 temperature=1.0, grad_loss=1.0, backward=True, nthreads=None, kl_beta=0.0,
                 kl_estimator=0, ref_logp=None, token_weight=None):

@@ -118,6 +118,33 @@ int oracle_task_adv_norm_ext(int64_t T_g, int32_t n_traj, int32_t n_task, int32_
                             task_std, adv_traj, adv_tok);
 }
 
+/*
+ * Sequence-level aggregation (App. B.2, GRPO objective: the mean over the
+ * responses of each response's token mean) as per-token weights of a packed
+ * micro-batch: count[j] = action tokens of trajectory j in it, n_seq =
+ * trajectories with count[j] > 0, w[t] = 1 / (n_seq * count[traj_id[t]]) on
+ * every action token with traj_id >= 0 (the quotient in fp64, rounded once to
+ * fp32), 0 on every other token.  Returns -1 (and skips the token) for a
+ * traj_id >= n_traj.
+ */
+int oracle_sequence_mean_weights(int64_t T, int32_t n_traj, const int32_t* traj_id,
+                                 const uint8_t* mask, int32_t* count, float* w) {
+  int rc = 0;
+  for (int32_t j = 0; j < n_traj; ++j) count[j] = 0;
+  for (int64_t t = 0; t < T; ++t) {
+    if (traj_id[t] >= n_traj) rc = -1;
+    else if (traj_id[t] >= 0 && mask[t]) count[traj_id[t]] += 1;
+  }
+  int64_t n_seq = 0;
+  for (int32_t j = 0; j < n_traj; ++j) n_seq += count[j] > 0;
+  for (int64_t t = 0; t < T; ++t) {
+    const int32_t j = traj_id[t];
+    w[t] = (j >= 0 && j < n_traj && mask[t]) ? (float)(1.0 / ((double)n_seq * (double)count[j]))
+                                             : 0.0f;
+  }
+  return rc;
+}
+
 static int task_adv_norm_impl(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_group,
                               const int32_t* traj_id, const uint8_t* mask,
                               const int32_t* traj_task, const int32_t* traj_group,
