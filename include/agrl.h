@@ -16,7 +16,9 @@
  *                          over them (App. B.2 PPO objective; App. A, the
  *                          DAPO objective's decoupled clip bounds and
  *                          token-level normalisation);
- *   agrl_policy_loss_bwd   dH and dW of that loss, recomputing the logits.
+ *   agrl_policy_loss_bwd   dH and dW of that loss, recomputing the logits;
+ *   agrl_sequence_mean_weights  per-token weights that turn the loss into the
+ *                          sequence-level mean of App. B.2's GRPO objective.
  *
  * Conventions for every entry point:
  *   - Array arguments are DEVICE pointers owned by the caller; the library
@@ -138,6 +140,30 @@ int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, int32_t n_gr
                        const float* reward, const agrl_options* opt, int32_t* act_count,
                        int64_t* task_count, float* task_mean, float* task_std, float* adv_traj,
                        float* adv_tok, void* stream);
+
+/*
+ * Per-token loss weights of the sequence-level aggregation.  App. B.2 writes
+ * GRPO's objective as a mean over the responses of a token mean within each
+ * response; for a packed micro-batch of T tokens this is
+ *   seq_count[j]    = action tokens of trajectory j in this micro-batch
+ *                     (action_mask != 0 and traj_id == j), int32
+ *   n_seq           = trajectories with seq_count[j] > 0
+ *   token_weight[t] = fp32(1 / (n_seq * seq_count[traj_id[t]])) on action
+ *                     tokens with traj_id >= 0 (the quotient is formed in
+ *                     fp64 and rounded once), 0 on every other token.
+ * Passed as agrl_options.token_weight to the policy-loss calls, the loss
+ * becomes -(1/n_seq) sum_j (1/seq_count[j]) sum_{t in j} (...).  A trajectory
+ * cut by the packing counts only its tokens in this micro-batch.
+ *   traj_id[T]       int32 trajectory of each token, -1 for padding (device)
+ *   action_mask[T]   uint8 (device)
+ *   seq_count[n_traj]  int32, written (device)
+ *   token_weight[T]  fp32, written (device)
+ * A traj_id >= n_traj sets ERR bit 2 of the device error word and the token
+ * is ignored.  T = 0 writes seq_count only.
+ */
+int agrl_sequence_mean_weights(int64_t T, int32_t n_traj, const int32_t* traj_id,
+                               const uint8_t* action_mask, int32_t* seq_count,
+                               float* token_weight, void* stream);
 
 /*
  * Bytes of device workspace the forward and backward calls need for a packed

@@ -8,12 +8,13 @@ allocates outputs and the workspace with torch.
 from ._binding import (AGRL_BF16, AGRL_F32, AgrlError, agrl_get_device_error,
                        agrl_options, agrl_policy_loss_bwd, agrl_policy_loss_fwd,
                        agrl_policy_loss_vocab_chunk, agrl_policy_loss_workspace_size,
-                       agrl_task_adv_norm, agrl_token_logprob,
+                       agrl_sequence_mean_weights, agrl_task_adv_norm, agrl_token_logprob,
                        agrl_token_logprob_workspace_size, lib)
-from .api import PolicyLoss, TokenLogprob, task_adv_norm
+from .api import PolicyLoss, TokenLogprob, sequence_mean_weights, task_adv_norm
 
 __all__ = ["AGRL_BF16", "AGRL_F32", "AgrlError", "agrl_options", "agrl_task_adv_norm",
            "agrl_policy_loss_workspace_size", "agrl_policy_loss_vocab_chunk",
            "agrl_policy_loss_fwd", "agrl_policy_loss_bwd",
            "agrl_token_logprob", "agrl_token_logprob_workspace_size",
-           "agrl_get_device_error", "lib", "PolicyLoss", "TokenLogprob", "task_adv_norm"]
+           "agrl_sequence_mean_weights", "agrl_get_device_error", "lib", "PolicyLoss",
+           "TokenLogprob", "sequence_mean_weights", "task_adv_norm"]

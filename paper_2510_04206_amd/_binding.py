@@ -57,6 +57,7 @@ _SIGS = {
     "agrl_token_logprob_workspace_size": (_c_sz, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
     "agrl_token_logprob": (_c_i32, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p,
                                     _c_p, _c_p, _c_sz, _c_p, _c_p, _c_p]),
+    "agrl_sequence_mean_weights": (_c_i32, [_c_i64, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "agrl_status_string": (ctypes.c_char_p, [_c_i32]),
     "agrl_last_error": (ctypes.c_char_p, []),
     "agrl_get_device_error": (_c_i32, [_c_p, _c_p]),
@@ -163,6 +164,13 @@ def agrl_token_logprob(T, max_act, d, V, dtype, H, W, token_id, action_mask, opt
     _check("agrl_token_logprob", lib().agrl_token_logprob(
         T, max_act, d, V, dtype, _ptr(H), _ptr(W), _ptr(token_id), _ptr(action_mask), _opts(opt),
         _ptr(workspace), ws_bytes, _ptr(logp), _ptr(lse), _stream(stream)))
+
+
+def agrl_sequence_mean_weights(T, n_traj, traj_id, action_mask, seq_count, token_weight,
+                               stream=None) -> None:
+    _check("agrl_sequence_mean_weights", lib().agrl_sequence_mean_weights(
+        T, n_traj, _ptr(traj_id), _ptr(action_mask), _ptr(seq_count), _ptr(token_weight),
+        _stream(stream)))
 
 
 def agrl_get_device_error(stream=None) -> int:

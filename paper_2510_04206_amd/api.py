@@ -27,6 +27,19 @@ def task_adv_norm(traj_id: torch.Tensor, action_mask: torch.Tensor, traj_task: t
     return out
 
 
+def sequence_mean_weights(traj_id: torch.Tensor, action_mask: torch.Tensor, n_traj: int,
+                          stream=None):
+    """agrl_sequence_mean_weights: (seq_count [n_traj] int32, token_weight [T] fp32), the
+    per-token weights of the sequence-level aggregation (pass token_weight's pointer as
+    agrl_options.token_weight)."""
+    dev = traj_id.device
+    seq_count = torch.empty(n_traj, dtype=torch.int32, device=dev)
+    token_weight = torch.empty(traj_id.numel(), dtype=torch.float32, device=dev)
+    B.agrl_sequence_mean_weights(traj_id.numel(), n_traj, traj_id, action_mask, seq_count,
+                                 token_weight, stream)
+    return seq_count, token_weight
+
+
 class PolicyLoss:
     """Forward/backward of the fused policy loss for one micro-batch shape.
 

@@ -207,6 +207,30 @@ int fail(int code, const char* msg) {
   return code;
 }
 
+// Sequence-level weights: every block counts the non-empty trajectories
+// (n_traj is small) and then weighs its tokens.
+__global__ __launch_bounds__(256) void seq_weight_kernel(int64_t T, int32_t n_traj,
+                                                         const int32_t* __restrict__ traj_id,
+                                                         const uint8_t* __restrict__ mask,
+                                                         const int32_t* __restrict__ seq_count,
+                                                         float* __restrict__ w) {
+  __shared__ int part[256 / 64];
+  int n = 0;
+  for (int j = threadIdx.x; j < n_traj; j += blockDim.x) n += seq_count[j] > 0;
+  for (int o = 32; o >= 1; o >>= 1) n += __shfl_xor(n, o);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = n;
+  __syncthreads();
+  const int n_seq = part[0] + part[1] + part[2] + part[3];
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < T;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int id = traj_id[t];
+    float v = 0.0f;
+    if (id >= 0 && id < n_traj && mask[t])
+      v = (float)(1.0 / ((double)n_seq * (double)seq_count[id]));
+    w[t] = v;
+  }
+}
+
 }  // namespace
 }  // namespace agrl
 
@@ -268,5 +292,34 @@ extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, i
   if (adv_tok && T_g > 0)
     hipLaunchKernelGGL(broadcast_kernel, dim3((unsigned)cdiv<int64_t>(T_g, 256)), dim3(256), 0, s,
                        T_g, n_traj, traj_id, action_mask, (const float*)adv_traj, adv_tok);
+  return hip_status(hipGetLastError());
+}
+
+extern "C" int agrl_sequence_mean_weights(int64_t T, int32_t n_traj, const int32_t* traj_id,
+                                          const uint8_t* action_mask, int32_t* seq_count,
+                                          float* token_weight, void* stream) {
+  using namespace agrl;
+  if (T < 0 || n_traj < 0) return fail(AGRL_E_SHAPE, "agrl_sequence_mean_weights: negative size");
+  if (T > ((int64_t)1 << 40))
+    return fail(AGRL_E_SHAPE, "agrl_sequence_mean_weights: T too large");
+  if (T > 0 && (!traj_id || !action_mask || !token_weight))
+    return fail(AGRL_E_NULL, "agrl_sequence_mean_weights: traj_id/action_mask/token_weight is NULL");
+  if (n_traj > 0 && !seq_count)
+    return fail(AGRL_E_NULL, "agrl_sequence_mean_weights: seq_count is NULL");
+  hipStream_t s = (hipStream_t)stream;
+  int* err = device_error_ptr();
+  if (!err) return hip_status(hipErrorInvalidSymbol);
+  if (n_traj > 0)
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, seq_count,
+                       (int64_t)n_traj, 0);
+  if (T > 0) {
+    const int64_t lanes = cdiv<int64_t>(T, kCountPerLane);
+    hipLaunchKernelGGL(count_kernel, dim3((unsigned)cdiv<int64_t>(lanes, 256)), dim3(256), 0, s,
+                       T, n_traj, traj_id, action_mask, seq_count, err);
+    const int64_t blocks = cdiv<int64_t>(T, 256);
+    hipLaunchKernelGGL(seq_weight_kernel, dim3((unsigned)(blocks < 1024 ? blocks : 1024)),
+                       dim3(256), 0, s, T, n_traj, traj_id, action_mask,
+                       (const int32_t*)seq_count, token_weight);
+  }
   return hip_status(hipGetLastError());
 }

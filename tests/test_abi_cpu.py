@@ -135,6 +135,17 @@ def test_adv_norm_argument_errors(L):
     assert f(10, 1, 1, 1, p, p, p, p, p, ctypes.byref(o), p, p, p, p, p, None, None) == E_FLAGS
 
 
+def test_sequence_mean_weights_argument_errors(L):
+    p = 1 << 12
+    f = L.agrl_sequence_mean_weights
+    assert f(-1, 1, p, p, p, p, None) == E_SHAPE
+    assert f(10, -1, p, p, p, p, None) == E_SHAPE
+    assert f(10, 1, None, p, p, p, None) == E_NULL
+    assert f(10, 1, p, None, p, p, None) == E_NULL
+    assert f(10, 1, p, p, p, None, None) == E_NULL
+    assert f(10, 1, p, p, None, p, None) == E_NULL     # seq_count needed when n_traj > 0
+
+
 def test_workspace_size(L):
     f = L.agrl_policy_loss_workspace_size
     assert f(0, 0, 64, 50, 0, None) == 0

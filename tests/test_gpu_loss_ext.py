@@ -104,3 +104,57 @@ def test_zero_beta_ignores_ref():
     b = run_gpu(P.PolicyLoss(w.T, w.d, w.V, w.H.dtype, max_act=w.n_act), d_in, adv)
     assert a["loss"] == b["loss"]
     np.testing.assert_array_equal(a["dW"], b["dW"])
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_sequence_mean_weights_bit_exact(k):
+    """agrl_sequence_mean_weights against the oracle on the workload's micro-batch
+    (the global stream's first T tokens): counts and fp32 weights bit-exact."""
+    import paper_2510_04206_amd as P
+    w = gen.config(k, tensors=False)
+    tid, mask = w.g_traj_id[: w.T], w.g_mask[: w.T]
+    log(f"seq-mean weights case workload {k}: T={w.T} n_traj={w.n_traj}")
+    c_ref, w_ref = oracle.sequence_mean_weights(tid, mask, w.n_traj)
+    cnt, wt = P.sequence_mean_weights(torch.from_numpy(np.ascontiguousarray(tid)).cuda(),
+                                      torch.from_numpy(np.ascontiguousarray(mask)).cuda(),
+                                      w.n_traj)
+    assert P.agrl_get_device_error() == 0
+    np.testing.assert_array_equal(cnt.cpu().numpy(), c_ref)
+    np.testing.assert_array_equal(wt.cpu().numpy(), w_ref)
+
+
+def test_sequence_mean_weights_edges():
+    import paper_2510_04206_amd as P
+    dev = torch.device("cuda")
+    log("seq-mean weights edges: padding only, empty, id out of range")
+    # only padding and observations: no trajectory present, every weight 0
+    tid = torch.tensor([-1, 0, 1, -1], dtype=torch.int32, device=dev)
+    mask = torch.tensor([1, 0, 0, 1], dtype=torch.uint8, device=dev)
+    cnt, wt = P.sequence_mean_weights(tid, mask, 2)
+    assert cnt.tolist() == [0, 0] and wt.tolist() == [0.0] * 4
+    # T = 0 still zeroes the counts
+    cnt, wt = P.sequence_mean_weights(torch.empty(0, dtype=torch.int32, device=dev),
+                                      torch.empty(0, dtype=torch.uint8, device=dev), 3)
+    assert cnt.tolist() == [0, 0, 0] and wt.numel() == 0
+    assert P.agrl_get_device_error() == 0
+    # an id >= n_traj is flagged and skipped
+    tid = torch.tensor([0, 5, 0, 1], dtype=torch.int32, device=dev)
+    mask = torch.ones(4, dtype=torch.uint8, device=dev)
+    cnt, wt = P.sequence_mean_weights(tid, mask, 2)
+    assert P.agrl_get_device_error() == 2
+    assert cnt.tolist() == [2, 1]
+    np.testing.assert_array_equal(wt.cpu().numpy(), np.float32([0.25, 0, 0.25, 0.5]))
+
+
+def test_library_weights_in_the_loss():
+    """The loss under the library's weights: identical weights to the host-built
+    ones, so identical GPU outputs."""
+    import paper_2510_04206_amd as P
+    w = gen.make(gen.small_spec(V=1800, d=128, dtype="bf16", name="seqlib"), seed=31)
+    tid = np.ascontiguousarray(w.g_traj_id[: w.T])
+    _, wt = P.sequence_mean_weights(torch.from_numpy(tid).cuda(),
+                                    torch.from_numpy(np.ascontiguousarray(w.mask)).cuda(),
+                                    w.n_traj)
+    host = seq_mean_weights(w)
+    np.testing.assert_array_equal(wt.cpu().numpy(), host)
+    _run(w, weight=host)
