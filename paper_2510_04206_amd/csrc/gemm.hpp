@@ -323,6 +323,15 @@ __device__ __forceinline__ void copy16(const void* g, uint32_t lds) {
 
 }  // namespace bf16k
 
+// The lane index computed afresh (from the exec mask, not from threadIdx.x), so
+// that quantities derived from it are formed where they are used instead of
+// being hoisted out of loops into spill slots
+__device__ __forceinline__ int fresh_lane() {
+  int v;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(v));
+  return v;
+}
+
 // Up to two independent problems in one launch (the backward's dH and dW).
 template <class Epi>
 struct GemmBatch {
@@ -412,7 +421,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)smem);
 
   for (;;) {
-    if (tid == 0) s_tile = atomicAdd(bat.queue + qi, 1);
+    if (wave == 0 && fresh_lane() == 0) s_tile = atomicAdd(bat.queue + qi, 1);
     __syncthreads();
     // the same value in every lane: make it a scalar, otherwise every quantity
     // derived from it (loop bounds, the copies' LDS base in M0) is treated as
@@ -441,25 +450,30 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     // lane i fetches chunk (i & 7) ^ swizzle(row) of row i / 8 (row-major: clamped
     // to the last valid row, those products are discarded by the epilogue;
     // stage-tiled: the chunk is already in place, the copy is 1 KiB contiguous)
+    // (the lane index is re-read here: lane-derived constants hoisted out of the
+    // tile loop end up in spill slots, and every reload is a round trip to memory
+    // that the streaming operands have evicted from the caches)
+    const int ln = fresh_lane();
     uint32_t offa[IPW], offb[IPW];
 #pragma unroll
     for (int b = 0; b < IPW; ++b) {
-      const int row = wave * 64 + b * RPI + (lane >> 3);
-      const int ch = ((lane & 7) ^ row_swizzle(row)) << 4;
-      offa[b] = g.a_tiled ? (uint32_t)(row * ROW + (lane & 7) * 16)
+      const int row = wave * 64 + b * RPI + (ln >> 3);
+      const int ch = ((ln & 7) ^ row_swizzle(row)) << 4;
+      offa[b] = g.a_tiled ? (uint32_t)(row * ROW + (ln & 7) * 16)
                           : (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
-      offb[b] = g.b_tiled ? (uint32_t)(row * ROW + (lane & 7) * 16)
+      offb[b] = g.b_tiled ? (uint32_t)(row * ROW + (ln & 7) * 16)
                           : (uint32_t)(min(row, N - 1 - n0) * ldb_b + ch);
     }
 
+    // (the LDS address is formed from scalars only, so it stays in SGPRs)
     auto copy = [&](int s, int q) {
       const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE);
       const int b = q % IPW;
       const uint32_t r0 = (uint32_t)(wave * 64 + b * RPI) * ROW;
       if (q < IPW)
-        copy16(a_base + s * a_ks + offa[b], __builtin_amdgcn_readfirstlane(st + r0));
+        copy16(a_base + s * a_ks + offa[b], st + r0);
       else
-        copy16(b_base + s * b_ks + offb[b], __builtin_amdgcn_readfirstlane(st + GBM * ROW + r0));
+        copy16(b_base + s * b_ks + offb[b], st + GBM * ROW + r0);
     };
 
     f32x16 acc[4][4];
@@ -541,7 +555,10 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __syncthreads();
-    epi(acc, m0, n0, tn, M, N, smem, wm, wn, lane, tid);
+    {
+      const int lane_e = fresh_lane();
+      epi(acc, m0, n0, tn, M, N, smem, wm, wn, lane_e, wave * 64 + lane_e);
+    }
     __syncthreads();
   }
 }
