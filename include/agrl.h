@@ -224,6 +224,8 @@ int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32_t V, int32
  * logits, the logit gradient is G[n, v] = g_n (1[v = y_n] - p[n, v]) / temperature and
  *   dH[T, d] fp32 = G W       (+0 rows for masked tokens)
  *   dW[V, d] fp32 = G^T H     (overwritten, or added to with opt->dw_accumulate)
+ * dH and dW must be 16-byte aligned (AGRL_E_UNSUPPORTED otherwise): their rows
+ * are written 16 bytes per lane.
  * The logits are recomputed tile by tile; G is rounded to `dtype` (bf16 for
  * AGRL_BF16) before the two products, which accumulate in fp32.
  */

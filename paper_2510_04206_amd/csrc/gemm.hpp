@@ -332,6 +332,12 @@ __device__ __forceinline__ int fresh_lane() {
   return v;
 }
 
+// Barrier that orders LDS accesses only: unlike __syncthreads() it does not
+// wait for this wave's global stores to complete.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Up to two independent problems in one launch (the backward's dH and dW).
 template <class Epi>
 struct GemmBatch {
@@ -557,7 +563,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     __syncthreads();
     {
       const int lane_e = fresh_lane();
-      epi(acc, m0, n0, tn, M, N, smem, wm, wn, lane_e, wave * 64 + lane_e);
+      epi.tile(acc, m0, n0, tn, M, N, smem, wm, wn, lane_e, wave * 64 + lane_e);
     }
     __syncthreads();
   }
@@ -785,9 +791,9 @@ struct EpiLseCols {
     }
   }
 
-  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
-                                             int N, uint8_t* smem, int wm, int wn, int lane,
-                                             int tid) const {
+  __device__ __forceinline__ void tile(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                       int N, uint8_t* smem, int wm, int wn, int lane,
+                                       int tid) const {
     int* sy = (int*)smem;
     f32x2* red = (f32x2*)(smem + 1024);
     // target row relative to the tile (-1: dead column; a target outside the
@@ -932,9 +938,9 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
     }
   }
 
-  __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
-                                             int N, uint8_t* smem, int wm, int wn, int lane,
-                                             int tid) const {
+  __device__ __forceinline__ void tile(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
+                                       int N, uint8_t* smem, int wm, int wn, int lane,
+                                       int tid) const {
     {
       const bool live = m0 + tid < M;
       // target column relative to the tile, -lse * log2(e) (-inf on dead rows, so
@@ -997,6 +1003,7 @@ struct EpiStore {
   const int32_t* row_map;   // nullable: output row of each tile row
   int32_t accumulate;
 
+  // simple kernel: direct stores from the accumulator layout
   __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
                                              int N, uint8_t* smem, int wm, int wn, int lane,
                                              int tid) const {
@@ -1021,6 +1028,65 @@ struct EpiStore {
         }
         if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
+  }
+
+  // bf16 kernel: two passes of 128 tile rows staged in LDS as fp32 rows of
+  // 1 KiB, each row then leaving as one 16-byte access per lane (read, added
+  // to and written back when accumulating, the reads of 16 rows in flight at a
+  // time).  Needs out 16-byte aligned and ldo a multiple of 4; N - n0 is a
+  // multiple of 64 (d is), so a lane's 4 columns are all in range or all out.
+  __device__ __forceinline__ void tile(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M, int N,
+                                       uint8_t* smem, int wm, int wn, int lane, int tid) const {
+    int* sr = (int*)(smem + EPI_META);
+    if (row_map) sr[tid] = (m0 + tid < M) ? row_map[m0 + tid] : 0;
+    float* st = (float*)smem;                     // [128][256] staged rows
+    const bool col_ok = n0 + 4 * lane < N;
+    const int wave = wm * 2 + wn;
+    if (accumulate)
+      passes<true>(acc, m0, n0, M, st, sr, wave, wm, wn, lane, col_ok);
+    else
+      passes<false>(acc, m0, n0, M, st, sr, wave, wm, wn, lane, col_ok);
+  }
+
+  template <bool ACC>
+  __device__ __forceinline__ void passes(const f32x16 (&acc)[4][4], int m0, int n0, int M,
+                                         float* st, const int* sr, int wave, int wm, int wn,
+                                         int lane, bool col_ok) const {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h) lds_barrier();                        // pass 0's rows have been read
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int lr = wm * 64 + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) st[lr * 256 + acc_col(wn, j, lane)] = acc[2 * h + ii][j][r];
+        }
+      lds_barrier();                               // rows staged (and sr written)
+      // staged row pr is tile row 64 h + pr (pr < 64) or 128 + 64 h + (pr - 64);
+      // wave w writes rows w, w + 4, ..., 16 at a time
+#pragma unroll
+      for (int k0 = 0; k0 < 32; k0 += 16) {
+        f32x4 old[16];
+        float* dst[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int pr = wave + 4 * (k0 + k);
+          const int tr = 64 * h + (pr < 64 ? pr : pr + 64);
+          const int64_t orow = row_map ? (int64_t)sr[tr] : (int64_t)(m0 + tr);
+          dst[k] = (m0 + tr < M && col_ok) ? out + orow * ldo + n0 + 4 * lane : nullptr;
+          if constexpr (ACC) old[k] = dst[k] ? *(const f32x4*)dst[k] : f32x4{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int pr = wave + 4 * (k0 + k);
+          f32x4 v = *(const f32x4*)(st + pr * 256 + 4 * lane);
+          if constexpr (ACC) v = v + old[k];
+          if (dst[k]) *(f32x4*)dst[k] = v;
+        }
+      }
+    }
   }
 };
 

@@ -973,6 +973,8 @@ extern "C" int agrl_policy_loss_bwd(int64_t T, int64_t max_act, int32_t d, int32
   if (rc) return rc;
   if (!dW || (T > 0 && (!dH || !lse || !logp)))
     return fail(AGRL_E_NULL, "agrl_policy_loss_bwd: lse/logp/dH/dW pointer is NULL");
+  if (((uintptr_t)dH | (uintptr_t)dW) % 16 != 0)
+    return fail(AGRL_E_UNSUPPORTED, "agrl_policy_loss_bwd: dH and dW must be 16-byte aligned");
   if (!isfinite(grad_loss)) return fail(AGRL_E_FLAGS, "agrl_policy_loss_bwd: grad_loss must be finite");
   hipStream_t s = (hipStream_t)stream;
   int* err = device_error_ptr();

@@ -98,6 +98,10 @@ def test_backward_argument_errors(L):
     assert L.agrl_policy_loss_bwd(10, 0, 64, 50, 0, 1 << 12, 1 << 12, 1 << 12, 1 << 12, 1 << 12,
                                   1 << 12, 0.2, 0.2, 0, None, 1 << 12, 1 << 12, float("inf"),
                                   1 << 12, need, 1 << 12, 1 << 12, None) == E_FLAGS
+    for dh, dw in ((4100, 1 << 12), (1 << 12, 4104)):      # rows are written 16 B per lane
+        assert L.agrl_policy_loss_bwd(10, 0, 64, 50, 0, 1 << 12, 1 << 12, 1 << 12, 1 << 12,
+                                      1 << 12, 1 << 12, 0.2, 0.2, 0, None, 1 << 12, 1 << 12, 1.0,
+                                      1 << 12, need, dh, dw, None) == E_UNSUP
 
 
 def test_token_logprob_argument_errors(L):
