@@ -841,7 +841,6 @@ struct LogitGradArgs {
   int64_t ldgt;
   float scale;
   int32_t col0;          // vocabulary index of this chunk's column 0
-  int32_t tiled;         // bf16: G and G^T are written stage-tiled (ldg, ldgt = padded K)
 };
 
 template <typename T>
@@ -968,29 +967,42 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
         stage_pass<false, h>(acc, n0, N, smem, wm, wn, lane);
       __syncthreads();
       // G: 128 rows of 512 bytes; pass rows 0..63 are tile rows 64h + r, rows
-      // 64..127 are tile rows 128 + 64h + (r - 64)
-#pragma unroll 4
-      for (int k = 0; k < 16; ++k) {
-        const int q = tid + GEMM_THREADS * k;
-        const int row = q >> 5, c16 = q & 31;
-        const int trow = 64 * h + (row < 64 ? row : row + 64);
-        const u32x4 v = *(const u32x4*)(smem + EPI_GS + row * EPI_G_ROW + c16 * 16);
-        const int64_t at = tiled ? tiled_index(m0 + trow, n0 + c16 * 8, ldg)
-                                 : (int64_t)(m0 + trow) * ldg + n0 + c16 * 8;
-        *(u32x4*)(G + at) = v;
+      // 64..127 are tile rows 128 + 64h + (r - 64).  Stage-tiled addresses: m0
+      // and n0 are multiples of 256, so a thread's block and chunk are fixed and
+      // only the row within the block changes from store to store.  Each loop
+      // reads all its LDS chunks before the first store, so the reads overlap.
+      {
+        const int c16 = tid & 31;
+        __bf16* base = G + (((int64_t)(m0 >> 8) * (ldg >> 6) + (n0 >> 6) + (c16 >> 3)) << 14);
+        u32x4 v[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          v[k] = *(const u32x4*)(smem + EPI_GS + ((tid >> 5) + 8 * k) * EPI_G_ROW + c16 * 16);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int row = (tid >> 5) + 8 * k;
+          const int trow = 64 * h + (row < 64 ? row : row + 64);
+          *(u32x4*)(base + ((trow << 6) + (((c16 & 7) ^ ((trow >> 1) & 7)) << 3))) = v[k];
+        }
       }
       // Gt: 256 rows (tile columns) of 16 chunks of 8 tile rows each
-#pragma unroll 4
-      for (int k = 0; k < 16; ++k) {
-        const int q = tid + GEMM_THREADS * k;
-        const int row = q >> 4, c16 = q & 15;
-        const int x = row & 31;
-        u32x4 v = *(const u32x4*)(smem + EPI_GTS + row * 256 + (((2 * c16) ^ x) >> 1) * 16);
-        if (x & 1) v = u32x4{v.z, v.w, v.x, v.y};
+      {
+        const int c16 = tid & 15;
         const int trow = 64 * h + (c16 < 8 ? 8 * c16 : 8 * c16 + 64);
-        const int64_t at = tiled ? tiled_index(n0 + row, m0 + trow, ldgt)
-                                 : (int64_t)(n0 + row) * ldgt + m0 + trow;
-        *(u32x4*)(Gt + at) = v;
+        __bf16* base = Gt + (((int64_t)(n0 >> 8) * (ldgt >> 6) + (m0 >> 6) + (trow >> 6)) << 14);
+        u32x4 v[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int row = (tid >> 4) + 16 * k;
+          const int x = row & 31;
+          v[k] = *(const u32x4*)(smem + EPI_GTS + row * 256 + (((2 * c16) ^ x) >> 1) * 16);
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int row = (tid >> 4) + 16 * k;
+          const u32x4 w = (row & 1) ? u32x4{v[k].z, v[k].w, v[k].x, v[k].y} : v[k];
+          *(u32x4*)(base + ((row << 6) + ((((trow & 63) >> 3) ^ ((row >> 1) & 7)) << 3))) = w;
+        }
       }
     }
   }
@@ -1078,12 +1090,13 @@ struct EpiStore {
           dst[k] = (m0 + tr < M && col_ok) ? out + orow * ldo + n0 + 4 * lane : nullptr;
           if constexpr (ACC) old[k] = dst[k] ? *(const f32x4*)dst[k] : f32x4{0, 0, 0, 0};
         }
+        f32x4 v[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) v[k] = *(const f32x4*)(st + (wave + 4 * (k0 + k)) * 256 + 4 * lane);
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
-          const int pr = wave + 4 * (k0 + k);
-          f32x4 v = *(const f32x4*)(st + pr * 256 + 4 * lane);
-          if constexpr (ACC) v = v + old[k];
-          if (dst[k]) *(f32x4*)dst[k] = v;
+          if constexpr (ACC) v[k] = v[k] + old[k];
+          if (dst[k]) *(f32x4*)dst[k] = v[k];
         }
       }
     }

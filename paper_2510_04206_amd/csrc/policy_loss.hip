@@ -769,7 +769,6 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       e.ldgt = L.A_pad;
       e.scale = c.inv_temp;
       e.col0 = (int32_t)v0;
-      e.tiled = tiled;
       launch_gemm<T>(&g, &e, 1, row_tiles * nv_tiles, (int32_t*)(ws + L.ctrl + 64), c.o,
                      PH_RECOMPUTE, -1, s);
     }
