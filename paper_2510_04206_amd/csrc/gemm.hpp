@@ -12,9 +12,9 @@
 // touches in 16 distinct bank groups.
 //
 // The grid is persistent (about one workgroup per compute unit, since a block
-// holds 128 KiB of LDS).  The row count M and the K extent may be read from
-// device memory, so a launch sized for an upper bound does only the work the
-// data needs without a host round trip.  Tile order: workgroups are dealt to
+// holds 128 KiB of LDS).  The row counts M and N and the K extent may be read
+// from device memory, so a launch sized for an upper bound does only the work
+// the data needs without a host round trip.  Tile order: workgroups are dealt to
 // the 8 XCDs round-robin, so each full round of tiles is renumbered to give
 // every XCD a contiguous run, and runs are laid out group_m row-tiles deep so
 // the 32 workgroups of an XCD share A and B panels in its L2.
