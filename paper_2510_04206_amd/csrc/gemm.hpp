@@ -316,8 +316,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 // prefetch).  The kernel orders copies and reads itself: vmcnt wait + barrier
 // before a buffer is read, barrier before it is refilled.  Nothing else in
 // these kernels uses M0.
-__device__ __forceinline__ void copy16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+__device__ __forceinline__ void copy16(const void* base, uint32_t off, uint32_t lds) {
+  // scalar base + 32-bit per-lane offset: no 64-bit address arithmetic per copy
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
+               "s"(lds)
                : "memory");
 }
 
@@ -477,9 +479,9 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       const int b = q % IPW;
       const uint32_t r0 = (uint32_t)(wave * 64 + b * RPI) * ROW;
       if (q < IPW)
-        copy16(a_base + s * a_ks + offa[b], st + r0);
+        copy16(a_base + s * a_ks, offa[b], st + r0);
       else
-        copy16(b_base + s * b_ks + offb[b], st + GBM * ROW + r0);
+        copy16(b_base + s * b_ks, offb[b], st + GBM * ROW + r0);
     };
 
     f32x16 acc[4][4];
