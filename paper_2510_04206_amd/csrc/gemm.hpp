@@ -316,10 +316,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 // prefetch).  The kernel orders copies and reads itself: vmcnt wait + barrier
 // before a buffer is read, barrier before it is refilled.  Nothing else in
 // these kernels uses M0.
+template <uint32_t LDS_OFF>
 __device__ __forceinline__ void copy16(const void* base, uint32_t off, uint32_t lds) {
-  // scalar base + 32-bit per-lane offset: no 64-bit address arithmetic per copy
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
-               "s"(lds)
+  // scalar base + 32-bit per-lane offset: no 64-bit address arithmetic per copy;
+  // M0 = lds + LDS_OFF in one scalar add
+  asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
+               "s"(lds), "n"(LDS_OFF)
                : "memory");
 }
 
@@ -474,14 +476,39 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     }
 
     // (the LDS address is formed from scalars only, so it stays in SGPRs)
-    auto copy = [&](int s, int q) {
-      const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE);
-      const int b = q % IPW;
-      const uint32_t r0 = (uint32_t)(wave * 64 + b * RPI) * ROW;
-      if (q < IPW)
-        copy16(a_base + s * a_ks, offa[b], st + r0);
+    // copy Q of stage s: the LDS address is the stage buffer and wave base (a
+    // scalar) plus a constant
+    auto copy = [&](int s, auto q_c) {
+      constexpr int Q = decltype(q_c)::value;
+      constexpr uint32_t b = Q % IPW;
+      const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE) + (uint32_t)(wave * 64 * ROW);
+      if constexpr (Q < IPW)
+        copy16<b * RPI * ROW>(a_base + s * a_ks, offa[b], st);
       else
-        copy16(b_base + s * b_ks, offb[b], st + GBM * ROW + r0);
+        copy16<GBM * ROW + b * RPI * ROW>(b_base + s * b_ks, offb[b], st);
+    };
+    // q is a constant at every call site once the loops are unrolled
+    auto copy_q = [&](int s, int q) {
+      static_assert(NCOPY == 16, "one case per copy");
+      switch (q) {
+        case 0: copy(s, std::integral_constant<int, 0>{}); break;
+        case 1: copy(s, std::integral_constant<int, 1>{}); break;
+        case 2: copy(s, std::integral_constant<int, 2>{}); break;
+        case 3: copy(s, std::integral_constant<int, 3>{}); break;
+        case 4: copy(s, std::integral_constant<int, 4>{}); break;
+        case 5: copy(s, std::integral_constant<int, 5>{}); break;
+        case 6: copy(s, std::integral_constant<int, 6>{}); break;
+        case 7: copy(s, std::integral_constant<int, 7>{}); break;
+        case 8: copy(s, std::integral_constant<int, 8>{}); break;
+        case 9: copy(s, std::integral_constant<int, 9>{}); break;
+        case 10: copy(s, std::integral_constant<int, 10>{}); break;
+        case 11: copy(s, std::integral_constant<int, 11>{}); break;
+        case 12: copy(s, std::integral_constant<int, 12>{}); break;
+        case 13: copy(s, std::integral_constant<int, 13>{}); break;
+        case 14: copy(s, std::integral_constant<int, 14>{}); break;
+        case 15: copy(s, std::integral_constant<int, 15>{}); break;
+        default: break;
+      }
     };
 
     f32x16 acc[4][4];
@@ -494,9 +521,11 @@ __global__ void __launch_bounds__(GEMM_THREADS)
 
     if (nk > 0) {
       // stage 0 whole; stage 1's slot 0..15 copies (stage 0 issues the rest)
-      for (int q = 0; q < NCOPY; ++q) copy(0, q);
+#pragma unroll
+      for (int q = 0; q < NCOPY; ++q) copy_q(0, q);
       if (nk > 1) {
-        for (int c = 0; c < NEARLY; ++c) copy(1, copy_order(c));
+#pragma unroll
+        for (int c = 0; c < NEARLY; ++c) copy_q(1, copy_order(c));
         wait_vmcnt<NEARLY>();      // stage 0 landed
       } else {
         wait_vmcnt<0>();
@@ -539,7 +568,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
               if constexpr (MORE) {
                 const int slot = 16 * (kk + 1) + q;
                 if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
-                  copy(kt + 1, copy_order(slot / CSTRIDE));
+                  copy_q(kt + 1, copy_order(slot / CSTRIDE));
               }
             } else {
               if constexpr (MORE) {
@@ -549,7 +578,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
                   fb[nxt][q - 4] = *(const bf16x8*)(sn + b_rd + (q - 4) * 32 * ROW + chk[0]);
               }
               if constexpr (REFILL) {
-                if (q % CSTRIDE == 0) copy(kt + NB, copy_order(q / CSTRIDE));
+                if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE));
               }
             }
             __builtin_amdgcn_sched_barrier(0);
