@@ -283,12 +283,14 @@ namespace bf16k {
 constexpr int SK = 64;                        // k per stage
 constexpr int ROW = SK * 2;                   // bytes per tile row per stage
 constexpr int STAGE = (GBM + GBN) * ROW;      // 64 KiB
+constexpr int HALF = GBM * ROW;               // one operand's part of a stage (32 KiB)
 constexpr int NB = 2;                         // stage buffers
 constexpr int KK = SK / 16;                   // 16-deep slices per stage
 constexpr int RPI = 1024 / ROW;               // tile rows per copy instruction (8)
 constexpr int IPW = 64 / RPI;                 // copy instructions per wave per operand (8)
 constexpr int NCOPY = 2 * IPW;                // per wave per stage (16)
 static_assert(NB * STAGE <= GEMM_LDS, "LDS");
+static_assert((NB - 1) * HALF + 3 * 32 * ROW < 65536, "fragment offsets fit a DS immediate");
 static_assert(NCOPY == 16, "one copy per MFMA of the last slice");
 // Copy schedule.  The 16 copies of stage s are spread over the MFMAs that
 // follow the barrier freeing their buffer: MFMA slot 0..15 is the last slice
@@ -392,7 +394,11 @@ __device__ __forceinline__ int queue_tile(int k, const QueueShare& s, int q, int
   return (s.full / 32) * (32 * nq) + (k - s.full) * nq + q;
 }
 
-template <class Epi>
+// EVEN: every problem's K is a multiple of 2 stages (a device-read K is rounded
+// up to one, the operands being zero-padded that far); the stage loop is then
+// unrolled by two and each stage knows its buffer at compile time, so every LDS
+// address of the loop is a base register plus an immediate.
+template <class Epi, bool EVEN>
 __global__ void __launch_bounds__(GEMM_THREADS)
     __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmBatch<Epi> bat) {
   using namespace bf16k;
@@ -411,7 +417,8 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     // device-read sizes are the same in every lane; keep them scalar (see below)
     Mp[p] = __builtin_amdgcn_readfirstlane(gp.m_dev ? *gp.m_dev : gp.M);
     Np[p] = __builtin_amdgcn_readfirstlane(gp.n_dev ? *gp.n_dev : gp.N);
-    Kp[p] = __builtin_amdgcn_readfirstlane(gp.k_dev ? cdiv(*gp.k_dev, SK) * SK : gp.K);
+    constexpr int KR = EVEN ? 2 * SK : SK;
+    Kp[p] = __builtin_amdgcn_readfirstlane(gp.k_dev ? cdiv(*gp.k_dev, KR) * KR : gp.K);
     tmp[p] = cdiv(Mp[p], GBM);
     tnp[p] = cdiv(Np[p], GBN);
     const int total = (p < bat.n && Mp[p] > 0 && Np[p] > 0) ? tmp[p] * tnp[p] : 0;
@@ -419,14 +426,18 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   }
 
   // fragment reads: lane l reads row (l & 31) of each 32-row block, chunk
-  // 2 kk + l / 32 of slice kk
+  // 2 kk + l / 32 of slice kk.  LDS holds the A halves of the two stage buffers
+  // first, then the B halves, so a read's buffer and block are an offset of at
+  // most 45 KiB from a per-slice base.
   const int frow = lane & 31;
   const int fsw = row_swizzle(frow);
-  const int a_rd = (wm * 128 + frow) * ROW;
-  const int b_rd = GBM * ROW + (wn * 128 + frow) * ROW;
-  int chk[KK];
+  int ra[KK], rb[KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) chk[kk] = ((kk * 2 + (lane >> 5)) ^ fsw) << 4;
+  for (int kk = 0; kk < KK; ++kk) {
+    const int chk = ((kk * 2 + (lane >> 5)) ^ fsw) << 4;
+    ra[kk] = (wm * 128 + frow) * ROW + chk;
+    rb[kk] = NB * HALF + (wn * 128 + frow) * ROW + chk;
+  }
   // LDS byte address of the stage buffers
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)smem);
 
@@ -476,40 +487,44 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     }
 
     // (the LDS address is formed from scalars only, so it stays in SGPRs)
-    // copy Q of stage s: the LDS address is the stage buffer and wave base (a
-    // scalar) plus a constant
-    auto copy = [&](int s, auto q_c) {
+    // copy Q of stage s into stage buffer BUF (or buf when BUF < 0): the LDS
+    // address is a scalar base plus a constant of the copy site
+    const uint32_t lds_w = lds0 + (uint32_t)(wave * 64 * ROW);
+    auto copy = [&](int s, auto q_c, auto buf_c, int buf) {
       constexpr int Q = decltype(q_c)::value;
+      constexpr int BUF = decltype(buf_c)::value;
       constexpr uint32_t b = Q % IPW;
-      const uint32_t st = lds0 + (uint32_t)((s % NB) * STAGE) + (uint32_t)(wave * 64 * ROW);
+      constexpr uint32_t fixed = BUF >= 0 ? (uint32_t)BUF * HALF : 0u;
+      const uint32_t base = BUF >= 0 ? lds_w : lds_w + (uint32_t)(buf * HALF);
       if constexpr (Q < IPW)
-        copy16<b * RPI * ROW>(a_base + s * a_ks, offa[b], st);
+        copy16<fixed + b * RPI * ROW>(a_base + s * a_ks, offa[b], base);
       else
-        copy16<GBM * ROW + b * RPI * ROW>(b_base + s * b_ks, offb[b], st);
+        copy16<NB * HALF + fixed + b * RPI * ROW>(b_base + s * b_ks, offb[b], base);
     };
     // q is a constant at every call site once the loops are unrolled
-    auto copy_q = [&](int s, int q) {
+    auto copy_q = [&](int s, int q, auto buf_c, int buf) {
       static_assert(NCOPY == 16, "one case per copy");
       switch (q) {
-        case 0: copy(s, std::integral_constant<int, 0>{}); break;
-        case 1: copy(s, std::integral_constant<int, 1>{}); break;
-        case 2: copy(s, std::integral_constant<int, 2>{}); break;
-        case 3: copy(s, std::integral_constant<int, 3>{}); break;
-        case 4: copy(s, std::integral_constant<int, 4>{}); break;
-        case 5: copy(s, std::integral_constant<int, 5>{}); break;
-        case 6: copy(s, std::integral_constant<int, 6>{}); break;
-        case 7: copy(s, std::integral_constant<int, 7>{}); break;
-        case 8: copy(s, std::integral_constant<int, 8>{}); break;
-        case 9: copy(s, std::integral_constant<int, 9>{}); break;
-        case 10: copy(s, std::integral_constant<int, 10>{}); break;
-        case 11: copy(s, std::integral_constant<int, 11>{}); break;
-        case 12: copy(s, std::integral_constant<int, 12>{}); break;
-        case 13: copy(s, std::integral_constant<int, 13>{}); break;
-        case 14: copy(s, std::integral_constant<int, 14>{}); break;
-        case 15: copy(s, std::integral_constant<int, 15>{}); break;
+        case 0: copy(s, std::integral_constant<int, 0>{}, buf_c, buf); break;
+        case 1: copy(s, std::integral_constant<int, 1>{}, buf_c, buf); break;
+        case 2: copy(s, std::integral_constant<int, 2>{}, buf_c, buf); break;
+        case 3: copy(s, std::integral_constant<int, 3>{}, buf_c, buf); break;
+        case 4: copy(s, std::integral_constant<int, 4>{}, buf_c, buf); break;
+        case 5: copy(s, std::integral_constant<int, 5>{}, buf_c, buf); break;
+        case 6: copy(s, std::integral_constant<int, 6>{}, buf_c, buf); break;
+        case 7: copy(s, std::integral_constant<int, 7>{}, buf_c, buf); break;
+        case 8: copy(s, std::integral_constant<int, 8>{}, buf_c, buf); break;
+        case 9: copy(s, std::integral_constant<int, 9>{}, buf_c, buf); break;
+        case 10: copy(s, std::integral_constant<int, 10>{}, buf_c, buf); break;
+        case 11: copy(s, std::integral_constant<int, 11>{}, buf_c, buf); break;
+        case 12: copy(s, std::integral_constant<int, 12>{}, buf_c, buf); break;
+        case 13: copy(s, std::integral_constant<int, 13>{}, buf_c, buf); break;
+        case 14: copy(s, std::integral_constant<int, 14>{}, buf_c, buf); break;
+        case 15: copy(s, std::integral_constant<int, 15>{}, buf_c, buf); break;
         default: break;
       }
     };
+    using BUF_RT = std::integral_constant<int, -1>;
 
     f32x16 acc[4][4];
 #pragma unroll
@@ -522,10 +537,11 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     if (nk > 0) {
       // stage 0 whole; stage 1's slot 0..15 copies (stage 0 issues the rest)
 #pragma unroll
-      for (int q = 0; q < NCOPY; ++q) copy_q(0, q);
+      for (int q = 0; q < NCOPY; ++q) copy_q(0, q, std::integral_constant<int, 0>{}, 0);
       if (nk > 1) {
 #pragma unroll
-        for (int c = 0; c < NEARLY; ++c) copy_q(1, copy_order(c));
+        for (int c = 0; c < NEARLY; ++c)
+          copy_q(1, copy_order(c), std::integral_constant<int, 1>{}, 1);
         wait_vmcnt<NEARLY>();      // stage 0 landed
       } else {
         wait_vmcnt<0>();
@@ -533,15 +549,19 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       __builtin_amdgcn_s_barrier();
       bf16x8 fa[2][4], fb[2][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[0][i] = *(const bf16x8*)(smem + a_rd + i * 32 * ROW + chk[0]);
+      for (int i = 0; i < 4; ++i) fa[0][i] = *(const bf16x8*)(smem + ra[0] + i * 32 * ROW);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[0][j] = *(const bf16x8*)(smem + b_rd + j * 32 * ROW + chk[0]);
+      for (int j = 0; j < 4; ++j) fb[0][j] = *(const bf16x8*)(smem + rb[0] + j * 32 * ROW);
 
-      auto stage = [&](int kt, auto refill_c, auto more_c) {
+      // P: stage kt's buffer (kt % NB), known at compile time when >= 0
+      auto stage = [&](int kt, auto refill_c, auto more_c, auto par_c) {
         constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
         constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
-        const uint8_t* st = smem + (kt % NB) * STAGE;
-        const uint8_t* sn = smem + ((kt + 1) % NB) * STAGE;
+        constexpr int P = decltype(par_c)::value;
+        using PC = std::integral_constant<int, P>;
+        using PN = std::integral_constant<int, P >= 0 ? (P ^ 1) : -1>;
+        const int pr = P >= 0 ? P : (kt % NB);               // this stage's buffer
+        const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
@@ -562,33 +582,49 @@ __global__ void __launch_bounds__(GEMM_THREADS)
                                                                 0, 0, 0);
             if (kk < KK - 1) {
               if (q < 4)
-                fa[nxt][q] = *(const bf16x8*)(st + a_rd + q * 32 * ROW + chk[kk + 1]);
+                fa[nxt][q] = *(const bf16x8*)(smem + ra[kk + 1] + cur_off + q * 32 * ROW);
               else if (q < 8)
-                fb[nxt][q - 4] = *(const bf16x8*)(st + b_rd + (q - 4) * 32 * ROW + chk[kk + 1]);
+                fb[nxt][q - 4] = *(const bf16x8*)(smem + rb[kk + 1] + cur_off + (q - 4) * 32 * ROW);
               if constexpr (MORE) {
                 const int slot = 16 * (kk + 1) + q;
                 if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
-                  copy_q(kt + 1, copy_order(slot / CSTRIDE));
+                  copy_q(kt + 1, copy_order(slot / CSTRIDE), PN{}, pr ^ 1);
               }
             } else {
               if constexpr (MORE) {
                 if (q < 4)
-                  fa[nxt][q] = *(const bf16x8*)(sn + a_rd + q * 32 * ROW + chk[0]);
+                  fa[nxt][q] = *(const bf16x8*)(smem + ra[0] + nxt_off + q * 32 * ROW);
                 else if (q < 8)
-                  fb[nxt][q - 4] = *(const bf16x8*)(sn + b_rd + (q - 4) * 32 * ROW + chk[0]);
+                  fb[nxt][q - 4] = *(const bf16x8*)(smem + rb[0] + nxt_off + (q - 4) * 32 * ROW);
               }
               if constexpr (REFILL) {
-                if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE));
+                if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), PC{}, pr);
               }
             }
             __builtin_amdgcn_sched_barrier(0);
           }
         }
       };
-      int kt = 0;
-      for (; kt + NB < nk; ++kt) stage(kt, std::true_type{}, std::true_type{});
-      for (; kt + 1 < nk; ++kt) stage(kt, std::false_type{}, std::true_type{});
-      stage(kt, std::false_type{}, std::false_type{});
+      using T_ = std::true_type;
+      using F_ = std::false_type;
+      if constexpr (EVEN) {
+        // nk even: pairs of stages with buffers 0 and 1, the last pair without
+        // copies of further stages
+        using P0 = std::integral_constant<int, 0>;
+        using P1 = std::integral_constant<int, 1>;
+        int kt = 0;
+        for (; kt + NB < nk; kt += 2) {
+          stage(kt, T_{}, T_{}, P0{});
+          stage(kt + 1, T_{}, T_{}, P1{});
+        }
+        stage(kt, F_{}, T_{}, P0{});
+        stage(kt + 1, F_{}, F_{}, P1{});
+      } else {
+        int kt = 0;
+        for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{}, BUF_RT{});
+        for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{}, BUF_RT{});
+        stage(kt, F_{}, F_{}, BUF_RT{});
+      }
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __syncthreads();

@@ -592,9 +592,16 @@ void launch_gemm(const GemmShape* g, const Epi* e, int n, int max_tiles, int32_t
     }
     b.n = n;
     b.queue = queue;
+    // every K a whole number of stage pairs (device-read ones are rounded up
+    // in the kernel, their operands being zero-padded to 256)
+    bool even = true;
+    for (int i = 0; i < n; ++i) even = even && (g[i].k_dev != nullptr || g[i].K % (2 * KStage<T>::BK) == 0);
     hipLaunchKernelGGL(zero_queue_kernel, dim3(1), dim3(64), 0, s, queue);
     if (ev) hipEventRecord(ev[2 * ph], s);
-    hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), dim3(grid), dim3(GEMM_THREADS), 0, s, b);
+    if (even)
+      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true>), dim3(grid), dim3(GEMM_THREADS), 0, s, b);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, b);
     if (ev) hipEventRecord(ev[2 * ph + 1], s);
     if (ev && ph2 >= 0) {
       hipEventRecord(ev[2 * ph2], s);
@@ -785,7 +792,8 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       g[0].b_tiled = tiled;
       g[0].m_dev = ctrl;
       g[0].N = c.d;
-      g[0].K = (int32_t)round_up(nv, KStage<T>::BK);
+      // (bf16: a whole number of stage pairs; G and W^T are zero up to Vc and V_pad)
+      g[0].K = (int32_t)round_up(nv, (tiled ? 2 : 1) * KStage<T>::BK);
       g[0].group_m = 8;
       g[1].A = Gt;
       g[1].lda = L.A_pad;
