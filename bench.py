@@ -188,8 +188,9 @@ def main():
                          "traffic, to scale the HBM counters of a profiling run)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(see DESIGN.md for how the work would shard).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path; "
+              "each GPU of a data-parallel job would run this step on its own micro-batch.",
+              file=sys.stderr)
         sys.exit(2)
 
     import paper_2510_04206_amd as P
