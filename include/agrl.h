@@ -69,11 +69,12 @@ typedef struct {
   float std_eps;         /* added to each std before dividing; 0 selects 1e-6 */
   float temperature;     /* logits are (H W^T) / temperature; 0 selects 1 */
   int32_t dw_accumulate; /* 0: dW is overwritten (default); 1: dW += gradient */
-  /* Bound on the backward's logit-gradient buffers (G and G^T of one vocabulary
-   * chunk, 2 * roundup(max_act, 256) * Vc * element size bytes).  The backward
-   * walks the vocabulary in equal chunks of Vc columns (a multiple of 256), as
-   * few as fit the bound; 0 selects 8 GiB.  The full T x V logit gradient is
-   * held only when it fits the bound. */
+  /* Bound on the backward's logit-gradient buffers for one vocabulary chunk:
+   * G, roundup(max_act, 256) * Vc * 2 bytes, for AGRL_BF16 (dW reads G
+   * transposed); G and G^T, twice that at 4 bytes per element, for AGRL_F32.
+   * The backward walks the vocabulary in equal chunks of Vc columns (a
+   * multiple of 256), as few as fit the bound; 0 selects 4 GiB.  The full
+   * T x V logit gradient is held only when it fits the bound. */
   int64_t g_chunk_bytes;
   /* Optional instrumentation: NULL, or a host array of 8 hipEvent_t.  The
    * library records events[2k] on `stream` just before and events[2k+1] just

@@ -32,13 +32,13 @@ constexpr int STAGE_BYTES = (GBM + GBN) * LDS_ROW;      // 64 KiB
 constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB of stage buffers
 // bf16 logit-gradient epilogue (two passes of 128 tile rows): G rows staged
 // row-major with 528-byte pitch (the two half-waves of a 16-bit store land in
-// different banks), the same values transposed as 256 rows of 256 bytes, and
-// three 256-entry per-row arrays
+// different banks); three 256-entry per-row arrays after the stage buffers
+// (the store epilogue stages a whole 128 KiB pass below them)
 constexpr int EPI_G_ROW = 528;
 constexpr int EPI_GS = 0;
-constexpr int EPI_GTS = 128 * EPI_G_ROW;                    // 67584
-constexpr int EPI_META = EPI_GTS + 256 * 256;               // 133120
-constexpr int EPI_STAGE_LDS = EPI_META + 3 * 1024;          // 136192 B
+constexpr int EPI_META = GEMM_LDS;                          // 131072
+constexpr int EPI_STAGE_LDS = EPI_META + 3 * 1024;          // 134144 B
+static_assert(EPI_GS + 128 * EPI_G_ROW <= EPI_META, "G staging below the per-row arrays");
 constexpr int BF16_KERNEL_LDS = EPI_STAGE_LDS > GEMM_LDS ? EPI_STAGE_LDS : GEMM_LDS;
 constexpr int GEMM_THREADS = 256;
 
@@ -65,9 +65,13 @@ struct GemmShape {
   int32_t K;               // multiple of BK (used when k_dev == nullptr)
   const int32_t* k_dev;    // K read on the device, rounded up to BK
   int32_t group_m;         // row-tiles per tile-order group
-  // bf16 kernel only: the operand is stored stage-tiled (see tiled_index) and
-  // lda / ldb is its padded K extent, a multiple of 64
-  int32_t a_tiled, b_tiled;
+  // bf16 kernel only.  a_tiled / b_tiled: the operand is stored stage-tiled,
+  // 1 in row-block order (tiled_index; lda / ldb = its padded K extent, a
+  // multiple of 64), 2 in column-block order (tiled_cm_index; lda / ldb = its
+  // padded row count, a multiple of 256).  a_trans: A is read transposed out
+  // of a column-block tiled matrix whose rows are the product's K and whose
+  // columns are the product's rows (lda = its padded row count).
+  int32_t a_tiled, b_tiled, a_trans;
 };
 
 // Stage-tiled bf16 layout of a matrix with rows r and K-columns k (K padded to
@@ -79,6 +83,17 @@ struct GemmShape {
 // 1 KiB of consecutive bytes), and a stage's rows share DRAM pages.
 __host__ __device__ __forceinline__ int64_t tiled_index(int64_t r, int64_t k, int64_t k_pad) {
   return (((r >> 8) * (k_pad >> 6) + (k >> 6)) << 14) + ((r & 255) << 6) +
+         ((((k & 63) >> 3) ^ ((r >> 1) & 7)) << 3) + (k & 7);
+}
+
+// The same blocks in column-block order: block (r / 256, k / 64) at index
+// (k / 64) * (r_pad / 256) + r / 256.  This is the layout of the backward's
+// logit gradient G (r = token, k = vocabulary entry).  dH reads it with K =
+// vocabulary (the stages of a 256-token tile are r_pad / 256 blocks apart); dW
+// reads it transposed with K = tokens (a 64-token stage lies 8 KiB further in
+// each of the tile's four block columns).  Both are uniform strides.
+__host__ __device__ __forceinline__ int64_t tiled_cm_index(int64_t r, int64_t k, int64_t r_pad) {
+  return (((k >> 6) * (r_pad >> 8) + (r >> 8)) << 14) + ((r & 255) << 6) +
          ((((k & 63) >> 3) ^ ((r >> 1) & 7)) << 3) + (k & 7);
 }
 
@@ -292,6 +307,16 @@ constexpr int NCOPY = 2 * IPW;                // per wave per stage (16)
 static_assert(NB * STAGE <= GEMM_LDS, "LDS");
 static_assert((NB - 1) * HALF + 3 * 32 * ROW < 65536, "fragment offsets fit a DS immediate");
 static_assert(NCOPY == 16, "one copy per MFMA of the last slice");
+// Transposed A (a_trans).  The stage's A half holds 64 k-rows of the tile's 256
+// rows of A, 512 bytes per k-row: the 64-byte window w (rows 32 w .. 32 w + 31)
+// of k-row k sits at window w ^ (k & 3).  A fragment (rows 32-block i, k slice
+// kk) is two transposing reads (ds_read_b64_tr_b16): within each 16-lane
+// group, lane s supplies k-row (s >> 2) and rows 4 (s & 3) .. + 3, and lane
+// 4a + b receives row 4a + b of k-rows 0..3 — in a 32-lane half the four k-rows
+// land in four distinct 64-byte bank windows.
+constexpr int TR_KROW = GBM * 2;                // bytes per k-row (512)
+static_assert((NB - 1) * HALF + (KK - 1) * 16 * TR_KROW + 4 * TR_KROW < 65536,
+              "transposed fragment offsets fit a DS immediate");
 // Copy schedule.  The 16 copies of stage s are spread over the MFMAs that
 // follow the barrier freeing their buffer: MFMA slot 0..15 is the last slice
 // of stage s - 2, slots 16..63 are slices 0..2 of stage s - 1, and copy c
@@ -325,6 +350,12 @@ __device__ __forceinline__ void copy16(const void* base, uint32_t off, uint32_t 
   asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base),
                "s"(lds), "n"(LDS_OFF)
                : "memory");
+}
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+__device__ __forceinline__ bf16x4 read_tr(const uint8_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
 }
 
 }  // namespace bf16k
@@ -397,10 +428,12 @@ __device__ __forceinline__ int queue_tile(int k, const QueueShare& s, int q, int
 // EVEN: every problem's K is a multiple of 2 stages (a device-read K is rounded
 // up to one, the operands being zero-padded that far); the stage loop is then
 // unrolled by two and each stage knows its buffer at compile time, so every LDS
-// address of the loop is a base register plus an immediate.
-template <class Epi, bool EVEN>
+// address of the loop is a base register plus an immediate.  ATR: a problem may
+// read A transposed (GemmShape::a_trans; EVEN launches only).
+template <class Epi, bool EVEN, bool ATR>
 __global__ void __launch_bounds__(GEMM_THREADS)
     __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmBatch<Epi> bat) {
+  static_assert(EVEN || !ATR, "transposed A in the stage-pair loop only");
   using namespace bf16k;
   __shared__ __attribute__((aligned(16))) uint8_t smem[BF16_KERNEL_LDS];
   __shared__ int s_tile;
@@ -460,13 +493,34 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     grouped_tile(L, p ? tmp[1] : tmp[0], p ? tnp[1] : tnp[0], g.group_m, tm, tn);
     const int64_t lda_b = g.lda * 2, ldb_b = g.ldb * 2;
     const int m0 = tm * GBM, n0 = tn * GBN;
-    // row-major: a tile starts at its first row and a stage advances 128 bytes;
-    // stage-tiled: a tile starts at its first 32 KiB block and a stage advances one
-    const uint8_t* a_base = (const uint8_t*)g.A + (g.a_tiled ? (int64_t)tm * (g.lda >> 6) * STAGE / 2
-                                                             : (int64_t)m0 * lda_b);
-    const uint8_t* b_base = (const uint8_t*)g.B + (g.b_tiled ? (int64_t)tn * (g.ldb >> 6) * STAGE / 2
-                                                             : (int64_t)n0 * ldb_b);
-    const int64_t a_ks = g.a_tiled ? STAGE / 2 : ROW, b_ks = g.b_tiled ? STAGE / 2 : ROW;
+    const bool atr = ATR && g.a_trans;
+    // where a tile starts and how far a stage advances.  Row-major: the tile's
+    // first row, 128 bytes.  Stage-tiled, row-block order: the tile's first
+    // 32 KiB block, one block.  Column-block order: the same, ld / 256 blocks.
+    // Transposed A: the tile's first block column, 64 k-rows of 128 bytes.
+    auto place = [&](int tiled, int64_t ld, int64_t ld_b, int t, int r0, int64_t& off,
+                     int64_t& ks) {
+      if (tiled == 2) {
+        off = (int64_t)t * HALF;
+        ks = (ld >> 8) * HALF;
+      } else if (tiled) {
+        off = (int64_t)t * (ld >> 6) * HALF;
+        ks = HALF;
+      } else {
+        off = (int64_t)r0 * ld_b;
+        ks = ROW;
+      }
+    };
+    int64_t a_off, a_ks, b_off, b_ks;
+    if (atr) {
+      a_off = (int64_t)tm * 4 * (g.lda >> 8) * HALF;
+      a_ks = SK * ROW;
+    } else {
+      place(g.a_tiled, g.lda, lda_b, tm, m0, a_off, a_ks);
+    }
+    place(g.b_tiled, g.ldb, ldb_b, tn, n0, b_off, b_ks);
+    const uint8_t* a_base = (const uint8_t*)g.A + a_off;
+    const uint8_t* b_base = (const uint8_t*)g.B + b_off;
     // copy q < 8 moves A rows [64 wave + 8 q, +8), q >= 8 the same rows of B;
     // lane i fetches chunk (i & 7) ^ swizzle(row) of row i / 8 (row-major: clamped
     // to the last valid row, those products are discarded by the epilogue;
@@ -484,6 +538,22 @@ __global__ void __launch_bounds__(GEMM_THREADS)
                           : (uint32_t)(min(row, M - 1 - m0) * lda_b + ch);
       offb[b] = g.b_tiled ? (uint32_t)(row * ROW + (ln & 7) * 16)
                           : (uint32_t)(min(row, N - 1 - n0) * ldb_b + ch);
+    }
+    if (atr) {
+      // transposed A: copy b of a wave fills k-rows 16 wave + 2 b, + 1 (the
+      // same LDS bytes as above); lane i lands in physical 16-byte chunk i & 31
+      // of its k-row, which holds rows 32 w + 8 (i & 3) .. + 7 of window
+      // w = ((i & 31) >> 2) ^ (k-row & 3).  In the source those rows are a
+      // 16-byte chunk of k-row (token) 64 s + kr of block column w / 2.
+#pragma unroll
+      for (int b = 0; b < IPW; ++b) {
+        const int kr = wave * 16 + 2 * b + (ln >> 5);
+        const int p = ln & 31;
+        const int w = (p >> 2) ^ (kr & 3);
+        // (lda <= 2^23 rows: at most 3 * 2^15 blocks of 32 KiB, within 32 bits)
+        offa[b] = (uint32_t)((w >> 1) * (uint32_t)((g.lda >> 8) * HALF) + kr * ROW +
+                             ((((w & 1) * 4 + (p & 3)) ^ ((kr >> 1) & 7)) << 4));
+      }
     }
 
     // (the LDS address is formed from scalars only, so it stays in SGPRs)
@@ -547,83 +617,116 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         wait_vmcnt<0>();
       }
       __builtin_amdgcn_s_barrier();
-      bf16x8 fa[2][4], fb[2][4];
+      // TR: A is read transposed (two half-fragment reads per 32-row block)
+      auto pipeline = [&](auto tr_c) {
+        constexpr bool TR = decltype(tr_c)::value;
+        // transposed A: lane l supplies k-row 8 (l >> 5) + ((l >> 2) & 3) of the
+        // slice and rows 16 ((l >> 4) & 1) + 4 (l & 3) .. + 3 of 32-block i
+        int ta[4];
+        if constexpr (TR) {
+          const int l = fresh_lane();
+          const int q4 = (l >> 2) & 3;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[0][i] = *(const bf16x8*)(smem + ra[0] + i * 32 * ROW);
+          for (int i = 0; i < 4; ++i)
+            ta[i] = (8 * (l >> 5) + q4) * TR_KROW + (4 * wm + (i ^ q4)) * 64 +
+                    32 * ((l >> 4) & 1) + 8 * (l & 3);
+        }
+        // the fragment read paired with MFMA q of a slice (slice kn, buffer
+        // offset off): A blocks first (two halves each when transposed), then B
+        auto frag = [&](int q, int kn, int off, bf16x8 (&fan)[4], bf16x8 (&fbn)[4]) {
+          if constexpr (TR) {
+            if (q < 8) {
+              const int i = q >> 1;
+              if (q & 1)
+                fan[i].hi = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW + 4 * TR_KROW);
+              else
+                fan[i].lo = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW);
+            } else if (q < 12) {
+              fbn[q - 8] = *(const bf16x8*)(smem + rb[kn] + off + (q - 8) * 32 * ROW);
+            }
+          } else {
+            if (q < 4)
+              fan[q] = *(const bf16x8*)(smem + ra[kn] + off + q * 32 * ROW);
+            else if (q < 8)
+              fbn[q - 4] = *(const bf16x8*)(smem + rb[kn] + off + (q - 4) * 32 * ROW);
+          }
+        };
+        bf16x8 fa[2][4], fb[2][4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[0][j] = *(const bf16x8*)(smem + rb[0] + j * 32 * ROW);
+        for (int q = 0; q < 16; ++q) frag(q, 0, 0, fa[0], fb[0]);
 
-      // P: stage kt's buffer (kt % NB), known at compile time when >= 0
-      auto stage = [&](int kt, auto refill_c, auto more_c, auto par_c) {
-        constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
-        constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
-        constexpr int P = decltype(par_c)::value;
-        using PC = std::integral_constant<int, P>;
-        using PN = std::integral_constant<int, P >= 0 ? (P ^ 1) : -1>;
-        const int pr = P >= 0 ? P : (kt % NB);               // this stage's buffer
-        const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
-        __builtin_amdgcn_sched_barrier(0);
+        // P: stage kt's buffer (kt % NB), known at compile time when >= 0
+        auto stage = [&](int kt, auto refill_c, auto more_c, auto par_c) {
+          constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
+          constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
+          constexpr int P = decltype(par_c)::value;
+          using PC = std::integral_constant<int, P>;
+          using PN = std::integral_constant<int, P >= 0 ? (P ^ 1) : -1>;
+          const int pr = P >= 0 ? P : (kt % NB);               // this stage's buffer
+          const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const int cur = kk & 1, nxt = cur ^ 1;
-          if (kk == KK - 1) {
-            if constexpr (MORE) {
-              // stage kt+1 landed (its copies are the only ones in flight)
-              wait_vmcnt<0>();
+          for (int kk = 0; kk < KK; ++kk) {
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk == KK - 1) {
+              if constexpr (MORE) {
+                // stage kt+1 landed (its copies are the only ones in flight)
+                wait_vmcnt<0>();
+              }
+              asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+              __builtin_amdgcn_s_barrier();
+              __builtin_amdgcn_sched_barrier(0);
             }
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            __builtin_amdgcn_s_barrier();
-            __builtin_amdgcn_sched_barrier(0);
-          }
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const int i = q >> 2, j = q & 3;
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
-                                                                0, 0, 0);
-            if (kk < KK - 1) {
-              if (q < 4)
-                fa[nxt][q] = *(const bf16x8*)(smem + ra[kk + 1] + cur_off + q * 32 * ROW);
-              else if (q < 8)
-                fb[nxt][q - 4] = *(const bf16x8*)(smem + rb[kk + 1] + cur_off + (q - 4) * 32 * ROW);
-              if constexpr (MORE) {
-                const int slot = 16 * (kk + 1) + q;
-                if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
-                  copy_q(kt + 1, copy_order(slot / CSTRIDE), PN{}, pr ^ 1);
+            for (int q = 0; q < 16; ++q) {
+              const int i = q >> 2, j = q & 3;
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
+                                                                  0, 0, 0);
+              if (kk < KK - 1) {
+                frag(q, kk + 1, cur_off, fa[nxt], fb[nxt]);
+                if constexpr (MORE) {
+                  const int slot = 16 * (kk + 1) + q;
+                  if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
+                    copy_q(kt + 1, copy_order(slot / CSTRIDE), PN{}, pr ^ 1);
+                }
+              } else {
+                if constexpr (MORE) frag(q, 0, nxt_off, fa[nxt], fb[nxt]);
+                if constexpr (REFILL) {
+                  if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), PC{}, pr);
+                }
               }
-            } else {
-              if constexpr (MORE) {
-                if (q < 4)
-                  fa[nxt][q] = *(const bf16x8*)(smem + ra[0] + nxt_off + q * 32 * ROW);
-                else if (q < 8)
-                  fb[nxt][q - 4] = *(const bf16x8*)(smem + rb[0] + nxt_off + (q - 4) * 32 * ROW);
-              }
-              if constexpr (REFILL) {
-                if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), PC{}, pr);
-              }
+              __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_sched_barrier(0);
           }
+        };
+        using T_ = std::true_type;
+        using F_ = std::false_type;
+        if constexpr (EVEN) {
+          // nk even: pairs of stages with buffers 0 and 1, the last pair without
+          // copies of further stages
+          using P0 = std::integral_constant<int, 0>;
+          using P1 = std::integral_constant<int, 1>;
+          int kt = 0;
+          for (; kt + NB < nk; kt += 2) {
+            stage(kt, T_{}, T_{}, P0{});
+            stage(kt + 1, T_{}, T_{}, P1{});
+          }
+          stage(kt, F_{}, T_{}, P0{});
+          stage(kt + 1, F_{}, F_{}, P1{});
+        } else {
+          int kt = 0;
+          for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{}, BUF_RT{});
+          for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{}, BUF_RT{});
+          stage(kt, F_{}, F_{}, BUF_RT{});
         }
       };
-      using T_ = std::true_type;
-      using F_ = std::false_type;
-      if constexpr (EVEN) {
-        // nk even: pairs of stages with buffers 0 and 1, the last pair without
-        // copies of further stages
-        using P0 = std::integral_constant<int, 0>;
-        using P1 = std::integral_constant<int, 1>;
-        int kt = 0;
-        for (; kt + NB < nk; kt += 2) {
-          stage(kt, T_{}, T_{}, P0{});
-          stage(kt + 1, T_{}, T_{}, P1{});
-        }
-        stage(kt, F_{}, T_{}, P0{});
-        stage(kt + 1, F_{}, F_{}, P1{});
+      if constexpr (ATR) {
+        if (atr)
+          pipeline(std::true_type{});
+        else
+          pipeline(std::false_type{});
       } else {
-        int kt = 0;
-        for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{}, BUF_RT{});
-        for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{}, BUF_RT{});
-        stage(kt, F_{}, F_{}, BUF_RT{});
+        pipeline(std::false_type{});
       }
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
@@ -902,9 +1005,9 @@ struct LogitGradArgs {
   const int32_t* y;
   const float* lse;
   const float* gs;       // dL/dlogp / temperature, per compacted row
-  T* G;
-  int64_t ldg;
-  T* Gt;
+  T* G;                  // fp32: row-major [rows][ldg]; bf16: column-block stage-tiled
+  int64_t ldg;           // fp32: row pitch; bf16: G's padded row count
+  T* Gt;                 // fp32 only: G transposed, row-major [cols][ldgt]
   int64_t ldgt;
   float scale;
   int32_t col0;          // vocabulary index of this chunk's column 0
@@ -954,11 +1057,10 @@ struct EpiLogitGrad<float> : LogitGradArgs<float> {
 
 // bf16 (pipelined kernel).  The tile is finished in two passes of 128 rows
 // (accumulator blocks i = 2h and 2h + 1 of both wave rows).  A pass stages its
-// G rows row-major and the same values transposed (256 rows of 128 bf16, in
-// 8-byte units placed at unit ^ (row & 31) so a wave's transposed stores hit
-// 64 distinct banks), then both leave LDS as full 128-byte lines.  The
-// exponent is evaluated in base 2 with the scale folded in:
-// exp(z - lse) = exp2(acc * scale * log2(e) - lse * log2(e)).
+// G rows row-major in LDS, then they leave as full 128-byte lines of G's
+// column-block stage-tiled layout (dW reads the same G transposed, so no
+// transposed copy is written).  The exponent is evaluated in base 2 with the
+// scale folded in: exp(z - lse) = exp2(acc * scale * log2(e) - lse * log2(e)).
 template <>
 struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
   template <bool FULL, int h>
@@ -996,8 +1098,6 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
           *(uint16_t*)(gs_at + EPI_G_ROW) = (uint16_t)(p01 >> 16);
           *(uint16_t*)(gs_at + 2 * EPI_G_ROW) = (uint16_t)p23;
           *(uint16_t*)(gs_at + 3 * EPI_G_ROW) = (uint16_t)(p23 >> 16);
-          const int unit = (lr >> 2) ^ (cl & 31);
-          *(u32x2*)(smem + EPI_GTS + cl * 256 + unit * 8) = u32x2{p01, p23};
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -1034,13 +1134,14 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
         stage_pass<false, h>(acc, n0, N, smem, wm, wn, lane);
       __syncthreads();
       // G: 128 rows of 512 bytes; pass rows 0..63 are tile rows 64h + r, rows
-      // 64..127 are tile rows 128 + 64h + (r - 64).  Stage-tiled addresses: m0
-      // and n0 are multiples of 256, so a thread's block and chunk are fixed and
-      // only the row within the block changes from store to store.  Each loop
-      // reads all its LDS chunks before the first store, so the reads overlap.
+      // 64..127 are tile rows 128 + 64h + (r - 64).  Column-block stage-tiled
+      // addresses: m0 and n0 are multiples of 256, so a thread's block and chunk
+      // are fixed and only the row within the block changes from store to
+      // store.  The loop reads all its LDS chunks before the first store, so the
+      // reads overlap.
       {
         const int c16 = tid & 31;
-        __bf16* base = G + (((int64_t)(m0 >> 8) * (ldg >> 6) + (n0 >> 6) + (c16 >> 3)) << 14);
+        __bf16* base = G + (((int64_t)((n0 >> 6) + (c16 >> 3)) * (ldg >> 8) + (m0 >> 8)) << 14);
         u32x4 v[16];
 #pragma unroll
         for (int k = 0; k < 16; ++k)
@@ -1050,25 +1151,6 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
           const int row = (tid >> 5) + 8 * k;
           const int trow = 64 * h + (row < 64 ? row : row + 64);
           *(u32x4*)(base + ((trow << 6) + (((c16 & 7) ^ ((trow >> 1) & 7)) << 3))) = v[k];
-        }
-      }
-      // Gt: 256 rows (tile columns) of 16 chunks of 8 tile rows each
-      {
-        const int c16 = tid & 15;
-        const int trow = 64 * h + (c16 < 8 ? 8 * c16 : 8 * c16 + 64);
-        __bf16* base = Gt + (((int64_t)(n0 >> 8) * (ldgt >> 6) + (m0 >> 6) + (trow >> 6)) << 14);
-        u32x4 v[16];
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const int row = (tid >> 4) + 16 * k;
-          const int x = row & 31;
-          v[k] = *(const u32x4*)(smem + EPI_GTS + row * 256 + (((2 * c16) ^ x) >> 1) * 16);
-        }
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const int row = (tid >> 4) + 16 * k;
-          const u32x4 w = (row & 1) ? u32x4{v[k].z, v[k].w, v[k].x, v[k].y} : v[k];
-          *(u32x4*)(base + ((row << 6) + ((((trow & 63) >> 3) ^ ((row >> 1) & 7)) << 3))) = w;
         }
       }
     }

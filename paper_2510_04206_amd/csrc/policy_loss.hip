@@ -444,7 +444,7 @@ struct Layout {
       blk_clip, H_act, part, Ht, Wt, G, Gt, fwd_total, total;
 };
 
-constexpr int64_t kDefaultChunkBytes = (int64_t)8 << 30;
+constexpr int64_t kDefaultChunkBytes = (int64_t)4 << 30;
 
 bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
                  const agrl_options& o, Layout* L) {
@@ -460,10 +460,12 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   if (L->nblk < 1) L->nblk = 1;
   L->tiles_v = (int32_t)(L->V_pad / GBN);
   L->merge_blocks = (int32_t)(L->A_pad / kMergeRows);
-  // vocabulary chunk of the backward: the widest multiple of 256 whose G and G^T
-  // fit the budget, then evened out over the chunks this needs
+  // vocabulary chunk of the backward: the widest multiple of 256 whose logit
+  // gradient buffers (bf16: G, read transposed by dW; fp32: G and G^T) fit the
+  // budget, then evened out over the chunks this needs
   const int64_t budget = o.g_chunk_bytes > 0 ? o.g_chunk_bytes : kDefaultChunkBytes;
-  int64_t vc_max = budget / (2 * L->A_pad * L->esize) / kRowPad * kRowPad;
+  const int64_t g_copies = dtype == AGRL_BF16 ? 1 : 2;
+  int64_t vc_max = budget / (g_copies * L->A_pad * L->esize) / kRowPad * kRowPad;
   if (vc_max < kRowPad) vc_max = kRowPad;
   const int64_t n_chunks = (L->V_pad + vc_max - 1) / vc_max;
   L->Vc = round_up((V + n_chunks - 1) / n_chunks, kRowPad);
@@ -500,7 +502,7 @@ bool make_layout(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype
   L->Ht = take(d_pad * A * L->esize);
   L->Wt = take(d_pad * L->V_pad * L->esize);
   L->G = take(A * (size_t)L->Vc * L->esize);
-  L->Gt = take((size_t)L->Vc * A * L->esize);
+  L->Gt = dtype == AGRL_BF16 ? L->G : take((size_t)L->Vc * A * L->esize);
   if (fwd_end > off) off = fwd_end;
   L->total = off;
   return true;
@@ -548,6 +550,8 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
   // every tile row offset and the G buffers use 32-bit row indices
   // operand rows are addressed as 32-bit offsets within a 256-row tile, so a row
   // of any operand (d, V or the padded action count, in elements) stays below 8M
+  // (this also bounds dW's transposed read of G: three block columns of at most
+  // 2^15 blocks of 32 KiB)
   if (round_up(max_act > 0 ? max_act : 1, kRowPad) > ((int64_t)1 << 23)) return bad(AGRL_E_SHAPE, "max_act too large");
   if (round_up(V, kRowPad) > ((int64_t)1 << 23) || d > (1 << 23)) return bad(AGRL_E_SHAPE, "V or d too large");
   Layout L;
@@ -594,14 +598,33 @@ void launch_gemm(const GemmShape* g, const Epi* e, int n, int max_tiles, int32_t
     b.queue = queue;
     // every K a whole number of stage pairs (device-read ones are rounded up
     // in the kernel, their operands being zero-padded to 256)
-    bool even = true;
-    for (int i = 0; i < n; ++i) even = even && (g[i].k_dev != nullptr || g[i].K % (2 * KStage<T>::BK) == 0);
+    bool even = true, atr = false;
+    for (int i = 0; i < n; ++i) {
+      even = even && (g[i].k_dev != nullptr || g[i].K % (2 * KStage<T>::BK) == 0);
+      atr = atr || g[i].a_trans;
+    }
     hipLaunchKernelGGL(zero_queue_kernel, dim3(1), dim3(64), 0, s, queue);
     if (ev) hipEventRecord(ev[2 * ph], s);
-    if (even)
-      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true>), dim3(grid), dim3(GEMM_THREADS), 0, s, b);
-    else
-      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, b);
+    // (transposed A is only built for the backward's dH + dW launch, whose K
+    // extents are always whole stage pairs; the callers guarantee it)
+    if constexpr (std::is_same<Epi, EpiStore>::value) {
+      if (atr && even)
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, true>), dim3(grid), dim3(GEMM_THREADS), 0,
+                           s, b);
+      else if (even)
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false>), dim3(grid), dim3(GEMM_THREADS), 0,
+                           s, b);
+      else
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
+                           0, s, b);
+    } else {
+      if (even)
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false>), dim3(grid), dim3(GEMM_THREADS), 0,
+                           s, b);
+      else
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
+                           0, s, b);
+    }
     if (ev) hipEventRecord(ev[2 * ph + 1], s);
     if (ev && ph2 >= 0) {
       hipEventRecord(ev[2 * ph2], s);
@@ -729,10 +752,11 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
   T* Ht = (T*)(ws + L.Ht);
   T* Wt = (T*)(ws + L.Wt);
   T* G = (T*)(ws + L.G);
-  T* Gt = (T*)(ws + L.Gt);
+  T* Gt = (T*)(ws + L.Gt);   // fp32 only
   // H_act^T [d][A_pad] (zero beyond the action rows) and W^T [d][V_pad] (zero
-  // beyond V); for bf16 both, and G and G^T, are stage-tiled: every stage of the
-  // two products below is a contiguous 32 KiB block per operand tile
+  // beyond V); for bf16 both, and G, are stage-tiled: every stage of the two
+  // products below is a contiguous 32 KiB block per operand tile (8 KiB in each
+  // of four blocks for dW's transposed read of G)
   constexpr int32_t tiled = std::is_same<T, __bf16>::value ? 1 : 0;
   const dim3 gh((unsigned)(L.A_pad / 64), (unsigned)cdiv(c.d, 64));
   const dim3 gw((unsigned)(L.V_pad / 64), (unsigned)cdiv(c.d, 64));
@@ -756,7 +780,7 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
   for (int64_t v0 = 0; v0 < c.V; v0 += L.Vc) {
     const int32_t nv = (int32_t)((c.V - v0) < L.Vc ? (c.V - v0) : L.Vc);
     const int nv_tiles = cdiv(nv, GBN);
-    {  // logits of the chunk -> G, Gt
+    {  // logits of the chunk -> G (and G^T for fp32)
       GemmShape g = {};
       g.A = ws + L.H_act;
       g.lda = c.d;
@@ -771,8 +795,8 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       e.lse = (const float*)(ws + L.lse_act);
       e.gs = (const float*)(ws + L.gs_act);
       e.G = G;
-      e.ldg = L.Vc;
-      e.Gt = Gt;
+      e.ldg = tiled ? L.A_pad : L.Vc;
+      e.Gt = tiled ? nullptr : Gt;
       e.ldgt = L.A_pad;
       e.scale = c.inv_temp;
       e.col0 = (int32_t)v0;
@@ -780,26 +804,28 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
                      PH_RECOMPUTE, -1, s);
     }
     {  // dH[idx] (+)= G W[v0 : v0 + nv] (K = the chunk's vocabulary columns) and
-       // dW[v0 : v0 + nv] = Gt H_act (K = action tokens), one launch, dH first:
-       // its tiles are the long ones
+       // dW[v0 : v0 + nv] = G^T H_act (K = action tokens), one launch, dH first:
+       // its tiles are the long ones.  bf16 G is column-block stage-tiled; dW
+       // reads it transposed (fp32 reads the separate G^T)
       GemmShape g[2] = {};
       g[0].A = G;
-      g[0].lda = L.Vc;
+      g[0].lda = tiled ? L.A_pad : L.Vc;
       // the chunk's first vocabulary column: a row offset, or whole 64-column blocks
       g[0].B = tiled ? (const void*)(Wt + v0 * 256) : (const void*)(Wt + v0);
       g[0].ldb = L.V_pad;
-      g[0].a_tiled = tiled;
+      g[0].a_tiled = tiled ? 2 : 0;
       g[0].b_tiled = tiled;
       g[0].m_dev = ctrl;
       g[0].N = c.d;
       // (bf16: a whole number of stage pairs; G and W^T are zero up to Vc and V_pad)
       g[0].K = (int32_t)round_up(nv, (tiled ? 2 : 1) * KStage<T>::BK);
       g[0].group_m = 8;
-      g[1].A = Gt;
+      g[1].A = tiled ? G : Gt;
       g[1].lda = L.A_pad;
       g[1].B = Ht;
       g[1].ldb = L.A_pad;
-      g[1].a_tiled = tiled;
+      g[1].a_tiled = tiled ? 2 : 0;
+      g[1].a_trans = tiled;
       g[1].b_tiled = tiled;
       g[1].M = nv;
       g[1].N = c.d;

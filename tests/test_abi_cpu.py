@@ -163,12 +163,21 @@ def test_workspace_size(L):
     from paper_2510_04206_amd._binding import agrl_options
     o = agrl_options(g_chunk_bytes=1 << 26)
     assert f(65536, 20000, 5120, 152064, 0, ctypes.byref(o)) < big
-    # default bound: G and G^T of one chunk stay within 8 GiB, so the whole
-    # T x V gradient is never held when it does not fit (64k action rows x 152064
-    # columns x 2 layouts x 2 B = 37 GiB)
-    full = 2 * 65536 * 152064 * 2
+    # default bound: one chunk's G (bf16; dW reads it transposed) stays within
+    # 4 GiB, so the whole T x V gradient is never held when it does not fit
+    # (64k action rows x 152064 columns x 2 B = 18.6 GiB)
+    full = 65536 * 152064 * 2
     assert f(65536, 65536, 5120, 152064, 0, None) < full
-    assert f(65536, 65536, 5120, 152064, 0, None) < (8 << 30) + (3 << 30)   # + H_act, H^T, W^T
+    assert f(65536, 65536, 5120, 152064, 0, None) < (4 << 30) + (3 << 30)   # + H_act, H^T, W^T
+    # the 32B-shaped micro-batch (22793 action tokens, padded to 23040) walks
+    # the vocabulary in two chunks of 76032 columns: G of 23040 x 93184 would
+    # be the widest that fits, 152064 needs two chunks, evened out
+    vc = L.agrl_policy_loss_vocab_chunk
+    assert vc(65536, 22793, 5120, 152064, 0, None) == 76032
+    # fp32 keeps G and G^T: half the columns per chunk for the same bound
+    o = agrl_options(g_chunk_bytes=2 * 1024 * 4 * 512)
+    assert vc(4096, 1000, 256, 4096, 1, ctypes.byref(o)) == 512
+    assert vc(4096, 1000, 256, 4096, 0, ctypes.byref(o)) == 2048
 
 
 def test_missing_library_fails_loudly(monkeypatch):
