@@ -1,5 +1,6 @@
 // Persistent "NT" GEMM on the gfx950 matrix cores: C[M, N] = A[M, K] * B[N, K]^T,
-// both operands K-contiguous, fp32 accumulation, with a fused epilogue functor.
+// both operands K-contiguous (the bf16 kernel can also read A transposed from
+// its stage-tiled storage), fp32 accumulation, with a fused epilogue functor.
 //
 // Block tile 256 x 256, 4 waves in a 2 x 2 arrangement, each wave owning a
 // 128 x 128 sub-tile as 4 x 4 blocks of 32 x 32 MFMA accumulators
@@ -997,9 +998,10 @@ __device__ __forceinline__ float to_store<float>(float v) {
   return v;
 }
 
-// Backward recompute: G = gs_n * (1[v == y_n] - exp(z - lse_n)), rounded to T,
-// written both as G[row][col] and transposed as Gt[col][row].  Rows >= M and
-// columns >= N are written as 0 (they pad the K extent of the next products).
+// Backward recompute: G = gs_n * (1[v == y_n] - exp(z - lse_n)), rounded to T.
+// fp32 writes it as G[row][col] and transposed as Gt[col][row]; bf16 writes G
+// only (stage-tiled).  Rows >= M and columns >= N are written as 0 (they pad
+// the K extent of the next products).
 template <typename T>
 struct LogitGradArgs {
   const int32_t* y;

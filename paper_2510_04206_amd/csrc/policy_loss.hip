@@ -7,9 +7,10 @@
 //           the matrix cores with a per-tile max / sum-exp epilogue (logits are
 //           never written) -> merge the vocabulary tiles into lse -> logp,
 //           ratio, clipped surrogate, fixed-order loss sum.
-// Backward: recompute the logit tiles, form G = dL/dz in bf16 (both layouts),
-//           then dW = G^T H and dH = G W on the matrix cores; the vocabulary is
-//           processed in chunks that bound the G buffers.
+// Backward: recompute the logit tiles, form G = dL/dz in bf16 (one stage-tiled
+//           layout, which dW reads transposed), then dW = G^T H and dH = G W on
+//           the matrix cores; the vocabulary is processed in chunks that bound
+//           the G buffer.
 #include <math.h>
 
 #include "../../include/agrl.h"
