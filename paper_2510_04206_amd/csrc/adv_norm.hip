@@ -22,27 +22,44 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
 // n_tau: each lane walks kCountPerLane consecutive tokens, adding runs of the
 // same trajectory; the wave then merges lanes that end on the same trajectory.
 // Integer atomics are exact, so the counts do not depend on the order.
+// VEC: traj_id and mask are 16-byte aligned, and a lane's whole run of tokens
+// is read with four 16-byte id loads and one 16-byte mask load.
+template <bool VEC>
 __global__ __launch_bounds__(256) void count_kernel(int64_t T_g, int32_t n_traj,
                                                     const int32_t* __restrict__ traj_id,
                                                     const uint8_t* __restrict__ mask,
                                                     int32_t* act_count, int* err) {
+  static_assert(kCountPerLane == 16, "one 16-byte mask load per lane");
   const int64_t t0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kCountPerLane;
   int cur = -1, cnt = 0;
-  for (int i = 0; i < kCountPerLane; ++i) {
-    const int64_t t = t0 + i;
-    if (t >= T_g) break;
-    const int id = traj_id[t];
+  auto token = [&](int id, bool m) {
     if (id >= n_traj) {
       set_error(err, ERR_TRAJ_ID);
-      continue;
+      return;
     }
-    if (id < 0 || !mask[t]) continue;
+    if (id < 0 || !m) return;
     if (id != cur) {
       if (cnt) atomicAdd(&act_count[cur], cnt);
       cur = id;
       cnt = 0;
     }
     ++cnt;
+  };
+  if (VEC && t0 + kCountPerLane <= T_g) {
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    i32x4 ids[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) ids[k] = *(const i32x4*)(traj_id + t0 + 4 * k);
+    const u32x4 mw = *(const u32x4*)(mask + t0);
+#pragma unroll
+    for (int i = 0; i < kCountPerLane; ++i)
+      token(ids[i >> 2][i & 3], (mw[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+  } else {
+    for (int i = 0; i < kCountPerLane; ++i) {
+      const int64_t t = t0 + i;
+      if (t >= T_g) break;
+      token(traj_id[t], mask[t] != 0);
+    }
   }
   const int lane = threadIdx.x & 63;
   for (;;) {
@@ -57,10 +74,13 @@ __global__ __launch_bounds__(256) void count_kernel(int64_t T_g, int32_t n_traj,
   }
 }
 
-__global__ void check_ids_kernel(int32_t n_traj, int32_t n_task, int32_t n_group,
-                                 const int32_t* traj_task, const int32_t* traj_group, int* err) {
+// Zero the per-trajectory counts and check the task / group ids, one launch.
+__global__ void prep_kernel(int32_t n_traj, int32_t n_task, int32_t n_group,
+                            const int32_t* traj_task, const int32_t* traj_group,
+                            int32_t* act_count, int* err) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= n_traj) return;
+  act_count[j] = 0;
   if (traj_task[j] < 0 || traj_task[j] >= n_task) set_error(err, ERR_TASK_ID);
   if (traj_group && (traj_group[j] < 0 || traj_group[j] >= n_group)) set_error(err, ERR_GROUP_ID);
 }
@@ -81,14 +101,9 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 // With drop_uniform, a group whose rewards are all equal is marked dropped by a
 // quiet NaN in a_hat (the task stage leaves such trajectories out and gives
 // them advantage 0).
-__global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_traj,
-                                                    const int32_t* __restrict__ traj_group,
-                                                    const float* __restrict__ reward,
-                                                    int32_t ddof, float eps, int32_t drop_uniform,
-                                                    float* a_hat) {
-  const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (g >= n_group) return;
-  const int lane = threadIdx.x & 63;
+__device__ void group_wave(int g, int lane, int32_t n_traj, const int32_t* __restrict__ traj_group,
+                           const float* __restrict__ reward, int32_t ddof, float eps,
+                           int32_t drop_uniform, float* a_hat) {
   float acc = 0.0f;
   int K = 0;
   for (int base = 0; base < n_traj; base += 64) {
@@ -135,21 +150,25 @@ __global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_t
     if (traj_group[tau] == g) a_hat[tau] = (reward[tau] - mu) / den;
 }
 
+__global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_traj,
+                                                    const int32_t* __restrict__ traj_group,
+                                                    const float* __restrict__ reward,
+                                                    int32_t ddof, float eps, int32_t drop_uniform,
+                                                    float* a_hat) {
+  const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (g < n_group)
+    group_wave(g, threadIdx.x & 63, n_traj, traj_group, reward, ddof, eps, drop_uniform, a_hat);
+}
+
 // Task stage: one wave per task; statistics of the token-level set, where
 // trajectory tau contributes its advantage with multiplicity n_tau.
 // src may alias adv_traj: each lane reads its own trajectories before writing them.
 // With drop_uniform, trajectories whose group stage left a NaN mark (dropped
 // groups) are not members of their task's set and get advantage 0.
-__global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_traj,
-                                                   const int32_t* __restrict__ traj_task,
-                                                   const int32_t* __restrict__ act_count,
-                                                   const float* src, int32_t ddof, float eps,
-                                                   int32_t drop_uniform, int64_t* task_count,
-                                                   float* task_mean, float* task_std,
-                                                   float* adv_traj) {
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (i >= n_task) return;
-  const int lane = threadIdx.x & 63;
+__device__ void task_wave(int i, int lane, int32_t n_traj, const int32_t* __restrict__ traj_task,
+                          const int32_t* __restrict__ act_count, const float* src, int32_t ddof,
+                          float eps, int32_t drop_uniform, int64_t* task_count, float* task_mean,
+                          float* task_std, float* adv_traj) {
   auto member = [&](int tau) {
     return traj_task[tau] == i && !(drop_uniform && isnan(src[tau]));
   };
@@ -193,13 +212,36 @@ __global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_tra
   }
 }
 
+__global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_traj,
+                                                   const int32_t* __restrict__ traj_task,
+                                                   const int32_t* __restrict__ act_count,
+                                                   const float* src, int32_t ddof, float eps,
+                                                   int32_t drop_uniform, int64_t* task_count,
+                                                   float* task_mean, float* task_std,
+                                                   float* adv_traj) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i < n_task)
+    task_wave(i, threadIdx.x & 63, n_traj, traj_task, act_count, src, ddof, eps, drop_uniform,
+              task_count, task_mean, task_std, adv_traj);
+}
+
+// VEC: traj_id, mask and adv_tok are 16-byte aligned and a thread handles 4
+// tokens with one 16-byte id load, one 4-byte mask load and one 16-byte store.
+template <bool VEC>
 __global__ void broadcast_kernel(int64_t T_g, int32_t n_traj, const int32_t* __restrict__ traj_id,
                                  const uint8_t* __restrict__ mask,
                                  const float* __restrict__ adv_traj, float* adv_tok) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T_g) return;
-  const int id = traj_id[t];
-  adv_tok[t] = (mask[t] && id >= 0 && id < n_traj) ? adv_traj[id] : 0.0f;
+  auto one = [&](int id, bool m) { return (m && id >= 0 && id < n_traj) ? adv_traj[id] : 0.0f; };
+  const int64_t t = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * (VEC ? 4 : 1);
+  if (VEC && t + 4 <= T_g) {
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    const i32x4 id = *(const i32x4*)(traj_id + t);
+    const uint32_t m = *(const uint32_t*)(mask + t);
+    *(f32x4*)(adv_tok + t) = f32x4{one(id[0], m & 0xFFu), one(id[1], (m >> 8) & 0xFFu),
+                                   one(id[2], (m >> 16) & 0xFFu), one(id[3], m >> 24)};
+    return;
+  }
+  for (int64_t u = t; u < T_g && u < t + (VEC ? 4 : 1); ++u) adv_tok[u] = one(traj_id[u], mask[u] != 0);
 }
 
 int fail(int code, const char* msg) {
@@ -269,29 +311,38 @@ extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, i
   int* err = device_error_ptr();
   if (!err) return hip_status(hipErrorInvalidSymbol);
 
-  if (n_traj > 0) {
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, act_count,
-                       (int64_t)n_traj, 0);
-    hipLaunchKernelGGL(check_ids_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, n_traj,
-                       n_task, n_group, traj_task, traj_group, err);
-  }
+  if (n_traj > 0)
+    hipLaunchKernelGGL(prep_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, n_traj, n_task,
+                       n_group, traj_task, traj_group, act_count, err);
+  const bool vec_in = (((uintptr_t)traj_id | (uintptr_t)action_mask) & 15) == 0;
   if (T_g > 0 && n_traj >= 0) {
     const int64_t lanes = cdiv<int64_t>(T_g, kCountPerLane);
-    hipLaunchKernelGGL(count_kernel, dim3((unsigned)cdiv<int64_t>(lanes, 256)), dim3(256), 0, s,
-                       T_g, n_traj, traj_id, action_mask, act_count, err);
+    const dim3 grid((unsigned)cdiv<int64_t>(lanes, 256));
+    if (vec_in)
+      hipLaunchKernelGGL(count_kernel<true>, grid, dim3(256), 0, s, T_g, n_traj, traj_id,
+                         action_mask, act_count, err);
+    else
+      hipLaunchKernelGGL(count_kernel<false>, grid, dim3(256), 0, s, T_g, n_traj, traj_id,
+                         action_mask, act_count, err);
   }
+  const int32_t ddof = (int32_t)o.std_ddof;
+  const int32_t drop = traj_group ? o.drop_uniform_groups : 0;
   if (traj_group && n_group > 0)
     hipLaunchKernelGGL(group_kernel, dim3(cdiv(n_group, 4)), dim3(256), 0, s, n_group, n_traj,
-                       traj_group, reward, (int32_t)o.std_ddof, eps, o.drop_uniform_groups,
-                       adv_traj);
+                       traj_group, reward, ddof, eps, drop, adv_traj);
   if (n_task > 0)
     hipLaunchKernelGGL(task_kernel, dim3(cdiv(n_task, 4)), dim3(256), 0, s, n_task, n_traj,
-                       traj_task, act_count, traj_group ? (const float*)adv_traj : reward,
-                       (int32_t)o.std_ddof, eps, traj_group ? o.drop_uniform_groups : 0, task_count,
-                       task_mean, task_std, adv_traj);
-  if (adv_tok && T_g > 0)
-    hipLaunchKernelGGL(broadcast_kernel, dim3((unsigned)cdiv<int64_t>(T_g, 256)), dim3(256), 0, s,
-                       T_g, n_traj, traj_id, action_mask, (const float*)adv_traj, adv_tok);
+                       traj_task, act_count, traj_group ? (const float*)adv_traj : reward, ddof,
+                       eps, drop, task_count, task_mean, task_std, adv_traj);
+  if (adv_tok && T_g > 0) {
+    if (vec_in && ((uintptr_t)adv_tok & 15) == 0)
+      hipLaunchKernelGGL(broadcast_kernel<true>, dim3((unsigned)cdiv<int64_t>(cdiv<int64_t>(T_g, 4), 256)),
+                         dim3(256), 0, s, T_g, n_traj, traj_id, action_mask,
+                         (const float*)adv_traj, adv_tok);
+    else
+      hipLaunchKernelGGL(broadcast_kernel<false>, dim3((unsigned)cdiv<int64_t>(T_g, 256)), dim3(256),
+                         0, s, T_g, n_traj, traj_id, action_mask, (const float*)adv_traj, adv_tok);
+  }
   return hip_status(hipGetLastError());
 }
 
@@ -314,8 +365,13 @@ extern "C" int agrl_sequence_mean_weights(int64_t T, int32_t n_traj, const int32
                        (int64_t)n_traj, 0);
   if (T > 0) {
     const int64_t lanes = cdiv<int64_t>(T, kCountPerLane);
-    hipLaunchKernelGGL(count_kernel, dim3((unsigned)cdiv<int64_t>(lanes, 256)), dim3(256), 0, s,
-                       T, n_traj, traj_id, action_mask, seq_count, err);
+    const dim3 grid((unsigned)cdiv<int64_t>(lanes, 256));
+    if ((((uintptr_t)traj_id | (uintptr_t)action_mask) & 15) == 0)
+      hipLaunchKernelGGL(count_kernel<true>, grid, dim3(256), 0, s, T, n_traj, traj_id,
+                         action_mask, seq_count, err);
+    else
+      hipLaunchKernelGGL(count_kernel<false>, grid, dim3(256), 0, s, T, n_traj, traj_id,
+                         action_mask, seq_count, err);
     const int64_t blocks = cdiv<int64_t>(T, 256);
     hipLaunchKernelGGL(seq_weight_kernel, dim3((unsigned)(blocks < 1024 ? blocks : 1024)),
                        dim3(256), 0, s, T, n_traj, traj_id, action_mask,
