@@ -84,8 +84,13 @@ def exported_symbols():
 
 
 def _ptr(t: Optional[torch.Tensor]):
+    """Device address of a contiguous GPU tensor (the ABI takes plain pointers)."""
     if t is None:
         return None
+    if not t.is_cuda:
+        raise ValueError("agrl: arrays must be GPU tensors (the ABI takes device pointers)")
+    if not t.is_contiguous():
+        raise ValueError("agrl: arrays must be contiguous (the ABI takes plain pointers)")
     return ctypes.c_void_p(t.data_ptr())
 
 

@@ -195,3 +195,12 @@ def test_product_never_touches_the_oracle():
             if fn.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
                 src = open(os.path.join(dirpath, fn)).read()
                 assert "oracle" not in src.lower(), fn
+
+
+def test_binding_rejects_host_tensors():
+    # the ABI takes device pointers: a host tensor is refused before any call
+    import torch
+    from paper_2510_04206_amd import _binding
+    with pytest.raises(ValueError):
+        _binding._ptr(torch.zeros(4))
+    assert _binding._ptr(None) is None

@@ -187,3 +187,13 @@ def test_argument_errors_on_gpu():
     with pytest.raises(P.AgrlError) as e:          # clip bound out of range
         pl.forward(H[:, :64].contiguous(), W[:, :64].contiguous(), ids, m, z, z)
     assert e.value.status == -4
+
+
+@pytest.mark.gpu
+def test_binding_rejects_strided_tensors():
+    from paper_2510_04206_amd import _binding
+    log("binding: non-contiguous tensor refused")
+    x = torch.zeros(8, 16, device="cuda").t()
+    with pytest.raises(ValueError):
+        _binding._ptr(x)
+    assert _binding._ptr(x.contiguous()) is not None
