@@ -74,15 +74,29 @@ class ClockSampler:
     """Samples the shader clock the driver reports (the starred line of
     pp_dpm_sclk in sysfs) from a background thread while the steps run: the
     sustained clock under this load, against which the published peak (quoted
-    at 2.4 GHz) is rescaled.  Reports None where the file is not readable."""
+    at 2.4 GHz) is rescaled, and the board power next to its cap (hwmon), which
+    shows whether that clock is set by the power limit.  Reports None where the
+    files are not readable."""
 
     def __init__(self, period_s: float = 0.01):
         import glob
         import threading
         files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
         self.path = files[0] if files else None
+        # board power (microwatts) and its cap from the same card's hwmon node
+        self.power_path = self.cap_path = None
+        if self.path:
+            hw = os.path.join(os.path.dirname(self.path), "hwmon", "hwmon*")
+            for name in ("power1_average", "power1_input"):
+                found = sorted(glob.glob(os.path.join(hw, name)))
+                if found and self._read_int(found[0]) is not None:
+                    self.power_path = found[0]
+                    break
+            caps = sorted(glob.glob(os.path.join(hw, "power1_cap")))
+            self.cap_path = caps[0] if caps else None
         self.period = period_s
         self.samples = []
+        self.power = []
         self._stop = threading.Event()
         self._thread = threading.Thread(target=self._run, daemon=True)
 
@@ -98,11 +112,23 @@ class ClockSampler:
             return None
         return None
 
+    @staticmethod
+    def _read_int(path):
+        try:
+            with open(path) as f:
+                return int(f.read().strip())
+        except (OSError, ValueError):
+            return None
+
     def _run(self):
         while not self._stop.is_set():
             v = self._read()
             if v is not None:
                 self.samples.append(v)
+            if self.power_path:
+                w = self._read_int(self.power_path)
+                if w is not None and w > 0:
+                    self.power.append(w * 1e-6)
             self._stop.wait(self.period)
 
     def __enter__(self):
@@ -121,6 +147,17 @@ class ClockSampler:
         a = np.array(self.samples, dtype=np.float64)
         return {"mean": float(a.mean()), "min": float(a.min()), "max": float(a.max()),
                 "samples": int(a.size), "source": self.path}
+
+    def power_summary(self):
+        """Board power in W over the timed steps, beside the cap the driver
+        enforces (None where hwmon does not expose them)."""
+        if not self.power:
+            return None
+        a = np.array(self.power, dtype=np.float64)
+        cap = self._read_int(self.cap_path) if self.cap_path else None
+        return {"mean": float(a.mean()), "min": float(a.min()), "max": float(a.max()),
+                "cap": cap * 1e-6 if cap else None, "samples": int(a.size),
+                "source": self.power_path}
 
 
 def kernel_sources_digest() -> str:
@@ -267,6 +304,7 @@ def main():
         end.record()
         torch.cuda.synchronize()
     sclk = clock.summary()
+    board_power = clock.power_summary()
     total_ms = start.elapsed_time(end)
     ms = total_ms / K
     if P.agrl_get_device_error() != 0:
@@ -359,6 +397,7 @@ def main():
                                      "and WRITE_SIZE scaled by a copy kernel of known size)",
                      "flops_per_launch": per_launch[dom]},
         "sclk_mhz": sclk,
+        "board_power_w": board_power,
     }
     if sclk:
         # the published peak is quoted at 2.4 GHz: the same fractions at the
