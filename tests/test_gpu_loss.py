@@ -55,6 +55,9 @@ SMALL = [
     ("fp32 V777 d64", dict(V=777, d=64, dtype="f32")),
     ("bf16 V300 d64 tiny", dict(V=300, d=64, dtype="bf16", n_tasks=1, n_groups=1, group_size=2,
                                  turns=(1, 2), obs=(1, 5), act=(1, 9))),
+    # d not a multiple of 256 (a partial last column tile in dH and dW)
+    ("bf16 V2048 d192", dict(V=2048, d=192, dtype="bf16")),
+    ("bf16 V1408 d320", dict(V=1408, d=320, dtype="bf16", n_tasks=3)),
 ]
 
 
@@ -77,6 +80,18 @@ def test_vocabulary_chunks_match_single_chunk():
     assert g1["loss"] == g3["loss"]
     np.testing.assert_array_equal(g1["dW"], g3["dW"])                    # dW rows do not mix chunks
     assert rel_fro(g3["dH"], g1["dH"]) < 1e-5
+
+
+def test_vocabulary_chunks_short_last_chunk():
+    """Four chunks, the last one 128 columns wide: the same result as one chunk,
+    and parity with the oracle."""
+    w = gen.make(gen.small_spec(V=1664, d=256, dtype="bf16", name="chunks wtr"), seed=8)
+    g1, _ = _run_case(w)
+    A_pad = (w.n_act + 255) // 256 * 256
+    g4, _ = _run_case(w, opt={"g_chunk_bytes": A_pad * 2 * 512})       # chunks of 512 columns
+    assert g1["loss"] == g4["loss"]
+    np.testing.assert_array_equal(g1["dW"], g4["dW"])
+    assert rel_fro(g4["dH"], g1["dH"]) < 1e-5
 
 
 def test_dw_accumulate():
