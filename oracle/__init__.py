@@ -4,7 +4,9 @@ Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 this package.  It shares no code with the HIP library and never imports it.
 The arithmetic lives in ``agrl_oracle.c`` (plain C: fp32 advantage
 normalisation in a fixed summation order, fp64 loss and gradients); this file
-only compiles it with gcc and marshals numpy arrays through ctypes.
+only compiles it with gcc and marshals numpy arrays through ctypes.  The one
+exception is ``blas.py``: the same fp64 forward with the logits from a library
+matmul, for whole batches at the full workload sizes.
 """
 from __future__ import annotations
 
@@ -188,3 +190,52 @@ def token_sample(H, W, token_id, mask, adv, old_logp, tokens, eps_lo=0.2, eps_hi
     if rc != 0:
         raise ValueError("oracle_token_sample: bad token index or id")
     return dict(lse=lse, logp=logp, g=g, dH=out_dH)
+
+
+def token_logprob_full(H, W, token_id, mask, temperature=1.0):
+    """fp64 logp and lse of every action token at any size (library matmul for
+    the logits; same definition as policy_loss's forward, App. B.1)."""
+    from .blas import token_logprob_fp64
+    logp, lse = token_logprob_fp64(H, W, token_id, mask, temperature=temperature)
+    return dict(logp=logp, lse=lse)
+
+
+def surrogate_terms(mask, adv, old_logp, logp, eps_lo=0.2, eps_hi=0.2, n_norm=0, grad_loss=1.0):
+    """Loss, clip counts and g = dL/dlogp of a micro-batch from fp64 log-probs of
+    its action tokens (App. B.2 PPO surrogate, App. A token-level mean)."""
+    lib = _load()
+    m = np.ascontiguousarray(mask, np.uint8)
+    T = m.shape[0]
+    loss = np.zeros(1)
+    n_clip = np.zeros(2, np.int64)
+    g = np.zeros(T)
+    f = lib.oracle_surrogate_terms
+    f.restype = ctypes.c_int
+    f(ctypes.c_int64(T), _p(m), _p(np.ascontiguousarray(adv, np.float32)),
+      _p(np.ascontiguousarray(old_logp, np.float32)), _p(np.ascontiguousarray(logp, np.float64)),
+      ctypes.c_double(eps_lo), ctypes.c_double(eps_hi), ctypes.c_int64(n_norm),
+      ctypes.c_double(grad_loss), _p(loss), _p(n_clip), _p(g))
+    return dict(loss=float(loss[0]), n_clip=n_clip, g=g)
+
+
+def dw_rows(H, W, token_id, mask, lse, g, rows, temperature=1.0, nthreads=None):
+    """Rows of dW = G^T H for the listed vocabulary entries, from every action
+    token's lse and dL/dlogp: fp64 [len(rows), d]."""
+    lib = _load()
+    Hn, hb = _as_input(H)
+    Wn, wb = _as_input(W)
+    assert hb == wb
+    T, d = Hn.shape
+    V = Wn.shape[0]
+    r = np.ascontiguousarray(rows, np.int64)
+    out = np.zeros((r.shape[0], d))
+    f = lib.oracle_dw_rows
+    f.restype = ctypes.c_int
+    rc = f(ctypes.c_int64(T), ctypes.c_int32(d), ctypes.c_int32(V), ctypes.c_int32(hb), _p(Hn),
+           _p(Wn), _p(np.ascontiguousarray(token_id, np.int32)),
+           _p(np.ascontiguousarray(mask, np.uint8)), ctypes.c_double(temperature),
+           _p(np.ascontiguousarray(lse, np.float64)), _p(np.ascontiguousarray(g, np.float64)),
+           _p(r), ctypes.c_int64(r.shape[0]), ctypes.c_int(_threads(nthreads)), _p(out))
+    if rc != 0:
+        raise ValueError("oracle_dw_rows: row or token id out of range")
+    return out

@@ -660,3 +660,60 @@ int oracle_token_sample(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const 
   free(act);
   return 0;
 }
+
+/*
+ * The surrogate, loss and dL/dlogp of every action token from log-probs the
+ * caller already holds (App. B.2 PPO objective; App. A DAPO token-level
+ * normalisation): the second half of the whole-batch forward above, for
+ * batches whose log-probs come from the fp64 full-logit pass in blas.py.
+ * logp is fp64 [T] (read on action tokens).  Outputs loss, n_clip[2] and
+ * g[T] (0 on masked tokens).
+ */
+int oracle_surrogate_terms(int64_t T, const uint8_t* mask, const float* adv, const float* old,
+                           const double* logp, double eps_lo, double eps_hi, int64_t n_norm,
+                           double grad_loss, double* loss, int64_t* n_clip, double* g) {
+  int64_t n_act = 0;
+  for (int64_t n = 0; n < T; ++n) n_act += mask[n] != 0;
+  double N = (double)(n_norm > 0 ? n_norm : n_act);
+  double sum = 0.0;
+  int64_t hi = 0, lo = 0;
+  for (int64_t n = 0; n < T; ++n) {
+    g[n] = 0.0;
+    if (!mask[n]) continue;
+    int clip;
+    sum += surrogate(logp[n], (double)old[n], (double)adv[n], eps_lo, eps_hi,
+                     N > 0 ? grad_loss / N : 0.0, &g[n], &clip);
+    hi += clip == 1;
+    lo += clip == -1;
+  }
+  *loss = N > 0 ? -sum / N : 0.0;
+  n_clip[0] = hi;
+  n_clip[1] = lo;
+  return 0;
+}
+
+/*
+ * Rows of dW for the listed vocabulary entries, given every action token's
+ * lse and dL/dlogp (as produced above): dW_v = sum_n g_n (1[v == y_n] - p_{n,v}) h_n
+ * over action tokens n, by the same per-row pass as the whole-batch backward.
+ * out_dW is [n_rows, d] fp64.
+ */
+int oracle_dw_rows(int64_t T, int32_t d, int32_t V, int32_t is_bf16, const void* H,
+                   const void* W, const int32_t* y, const uint8_t* mask, double temperature,
+                   const double* lse, const double* g, const int64_t* rows, int64_t n_rows,
+                   int nthreads, double* out_dW) {
+  for (int64_t i = 0; i < n_rows; ++i)
+    if (rows[i] < 0 || rows[i] >= V) return -1;
+  for (int64_t n = 0; n < T; ++n)
+    if (mask[n] && (y[n] < 0 || y[n] >= V)) return -1;
+  job_t J;
+  fill_job(&J, T, d, V, is_bf16, H, W, y, mask, NULL, NULL, 0.0, 0.0, 1.0 / temperature,
+           nthreads);
+  J.lse = (double*)lse;
+  J.g = (double*)g;
+  J.rows = rows;
+  J.n_rows = n_rows;
+  J.dW = out_dW;
+  run_threads(&J, dw_worker);
+  return 0;
+}
