@@ -35,8 +35,13 @@
  *     outputs are logp = lse = 0 and dH row = +0.
  *   - Faults found on the device (an id out of range, more action tokens
  *     than max_act) set bits in a per-device error word; read it with
- *     agrl_get_device_error.  Outputs of such a call are unspecified (loss is
- *     NaN for the max_act case).
+ *     agrl_get_device_error.  An action token whose token_id lies outside
+ *     [0, V) poisons the call's outputs, so that a caller who does not read
+ *     the word still sees the fault: that token's logp and lse are NaN, the
+ *     loss is NaN, and in the backward its logit-gradient row is NaN, which
+ *     makes its dH row and every row of dW NaN.  Other tokens' logp and lse
+ *     are unaffected.  With more action tokens than max_act the loss is NaN
+ *     and the other outputs are unspecified.
  *   - Results are deterministic: every reduction has a fixed order, no
  *     floating-point atomics are used.
  */

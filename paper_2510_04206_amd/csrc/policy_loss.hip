@@ -88,6 +88,7 @@ __global__ __launch_bounds__(1024) void scan_offsets_kernel(int32_t nblk,
       ctrl[1] = 0;
     }
     ctrl[2] = total;
+    ctrl[3] = 0;        // set by the scatter when an action token's id is out of range
   }
 }
 
@@ -103,6 +104,7 @@ struct ScatterArgs {
   const float* logp_in;     // backward only
   const int32_t* blk_off;
   const int32_t* ctrl;
+  int32_t* bad_id;          // ctrl[3]: 1 once an action token's id is out of range
   int64_t cap;              // rows allocated for compacted arrays
   int32_t* idx;
   int32_t* y_act;
@@ -158,8 +160,16 @@ __global__ __launch_bounds__(kScanThreads) void scan_scatter_kernel(ScatterArgs 
       }
       continue;
     }
-    const int y = a.token_id[t];
-    if (y < 0 || y >= a.V) set_error(a.err, ERR_TOKEN_ID);
+    const int y_in = a.token_id[t];
+    // an id outside the vocabulary poisons the call: the token is kept with
+    // id -1 (it matches no logit), its logp / lse become NaN in the merge, its
+    // logit-gradient row NaN in the backward, and the loss NaN
+    const bool bad = y_in < 0 || y_in >= a.V;
+    const int y = bad ? -1 : y_in;
+    if (bad) {
+      set_error(a.err, ERR_TOKEN_ID);
+      *a.bad_id = 1;
+    }
     if (ok && pos < a.cap) {
       a.idx[pos] = (int32_t)t;
       a.y_act[pos] = y;
@@ -183,7 +193,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_scatter_kernel(ScatterArgs 
           g += scale * a.kl_beta * dkl;
         }
         a.lse_act[pos] = a.lse_in[t];
-        a.gs_act[pos] = g * a.inv_temp;
+        a.gs_act[pos] = bad ? NAN : g * a.inv_temp;
       } else {
         a.ref_act[pos] = a.ref_logp ? a.ref_logp[t] : 0.0f;
         a.w_act[pos] = a.token_weight ? a.token_weight[t] : 0.0f;
@@ -294,6 +304,7 @@ struct MergeArgs {
   const f32x2* part;
   int64_t ld_part;
   const float* zy;
+  const int32_t* y_act;    // -1 marks an action token whose id was out of range
   const float* old_act;
   const float* adv_act;
   const float* ref_act;
@@ -338,8 +349,9 @@ __global__ __launch_bounds__(256) void merge_loss_kernel(MergeArgs a) {
     float sum = 0.0f;
     for (int w = 0; w < 4; ++w)
       if (wpart[w][lane].y > 0.0f) sum += wpart[w][lane].y * expf(wpart[w][lane].x - mm);
-    const float lse = mm + logf(sum);
-    const float logp = a.zy[n] - lse;
+    const bool bad = a.y_act[n] < 0;
+    const float lse = bad ? NAN : mm + logf(sum);
+    const float logp = bad ? NAN : a.zy[n] - lse;
     const float A = a.adv_act[n];
     const float rho = expf(logp - a.old_act[n]);
     const float rc = fminf(fmaxf(rho, 1.0f - a.eps_lo), 1.0f + a.eps_hi);
@@ -398,7 +410,7 @@ __global__ __launch_bounds__(256) void finalize_loss_kernel(int32_t nblk, const 
     const int n_act = ctrl[0];
     const double N = n_norm > 0 ? (double)n_norm : (double)n_act;
     float L = weighted ? (float)(-ssum[0]) : (N > 0 ? (float)(-ssum[0] / N) : 0.0f);
-    if (ctrl[1]) L = NAN;
+    if (ctrl[1] || ctrl[3]) L = NAN;
     *loss = L;
     if (n_clip) {
       n_clip[0] = shi[0];
@@ -665,6 +677,7 @@ int compact(const Common& c, const Layout& L, uint8_t* ws, const uint8_t* mask,
   a.logp_in = logp_in;
   a.blk_off = (const int32_t*)(ws + L.blk_off);
   a.ctrl = ctrl;
+  a.bad_id = ctrl + 3;
   a.cap = L.A_pad;
   a.idx = (int32_t*)(ws + L.idx);
   a.y_act = (int32_t*)(ws + L.y_act);
@@ -907,6 +920,7 @@ extern "C" int agrl_policy_loss_fwd(int64_t T, int64_t max_act, int32_t d, int32
   m.part = (const f32x2*)(ws + L.part);
   m.ld_part = L.A_pad;
   m.zy = (const float*)(ws + L.zy);
+  m.y_act = (const int32_t*)(ws + L.y_act);
   m.old_act = (const float*)(ws + L.old_act);
   m.adv_act = (const float*)(ws + L.adv_act);
   m.idx = (const int32_t*)(ws + L.idx);
@@ -973,6 +987,7 @@ extern "C" int agrl_token_logprob(int64_t T, int64_t max_act, int32_t d, int32_t
   m.part = (const f32x2*)(ws + L.part);
   m.ld_part = L.A_pad;
   m.zy = (const float*)(ws + L.zy);
+  m.y_act = (const int32_t*)(ws + L.y_act);
   m.old_act = (const float*)(ws + L.old_act);
   m.adv_act = (const float*)(ws + L.adv_act);
   m.idx = (const int32_t*)(ws + L.idx);
