@@ -62,9 +62,14 @@ def compare_loss(gpu, ref, w_mask, adv, old, eps_lo, eps_hi, *, loss_rel=1e-3, l
     lse = gpu["lse"]
     # masked positions are exactly 0
     assert np.all(logp[~m] == 0) and np.all(lse[~m] == 0)
+    L, R = gpu["loss"], ref["loss"]
+    if m.any():
+        e_lse = float(np.abs(lse[m] - ref["lse"][m]).max())
+        e_lp = float(np.abs(logp[m] - ref["logp"][m]).max())
+        log(f"  max |d lse| {e_lse:.3e}  max |d logp| {e_lp:.3e}  (atol {lp_atol:.1e}); "
+            f"loss rel err {abs(L - R) / max(abs(R), 1e-30):.3e}")
     np.testing.assert_allclose(lse[m], ref["lse"][m], rtol=1e-5, atol=lp_atol)
     np.testing.assert_allclose(logp[m], ref["logp"][m], rtol=1e-5, atol=lp_atol)
-    L, R = gpu["loss"], ref["loss"]
     assert abs(L - R) <= loss_rel * abs(R) + 1e-7, (L, R)
     flips = near_clip(ref["logp"], old, adv, m, eps_lo, eps_hi)
     assert np.abs(np.asarray(gpu["n_clip"]) - ref["n_clip"]).sum() <= flips.sum()

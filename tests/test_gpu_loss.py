@@ -94,6 +94,37 @@ def test_vocabulary_chunks_short_last_chunk():
     assert rel_fro(g4["dH"], g1["dH"]) < 1e-5
 
 
+def _launch_tiles(n_act, V, d, vc):
+    """Tiles of each matrix-core launch: forward (vocabulary x tokens), recompute
+    per chunk (tokens x chunk columns), dH + dW per chunk (tokens x d, chunk x d)."""
+    t = lambda x: -(-x // 256)
+    chunks = [min(vc, V - v0) for v0 in range(0, V, vc)]
+    return (t(V) * t(n_act), [t(n_act) * t(c) for c in chunks],
+            [t(n_act) * t(d) + t(c) * t(d) for c in chunks])
+
+
+@pytest.mark.timeout(600)
+def test_whole_batch_multi_round_three_chunks():
+    """A whole batch large enough for the persistent schedule to run several
+    rounds of 256 tiles per launch (every workgroup takes several tiles, the
+    queues' full-round and final partial-round branches both run), with three
+    vocabulary chunks, the last one ragged: every output element against the
+    oracle's whole batch."""
+    import paper_2510_04206_amd as P
+    w = gen.make(gen.small_spec(V=131000, d=384, dtype="bf16", n_tasks=3, n_groups=2,
+                                group_size=7, name="whole batch V131000 d384"),
+                 seed=32, device="cuda")
+    A_pad = -(-w.n_act // 256) * 256
+    opt = {"g_chunk_bytes": 49152 * A_pad * 2}
+    vc = P.PolicyLoss(w.T, w.d, w.V, w.H.dtype, max_act=w.n_act, opt=opt).vocab_chunk
+    fwd, rec, bwd = _launch_tiles(w.n_act, w.V, w.d, vc)
+    log(f"  vocab chunk {vc}; tiles: forward {fwd}, recompute {rec}, dH + dW {bwd}")
+    # ragged in every dimension: tokens, vocabulary, the last chunk and d
+    assert len(rec) == 3 and w.V % 256 and (w.V - 2 * vc) % 256 and w.n_act % 256 and w.d % 256
+    assert fwd >= 1024 and min(rec) >= 1024 and min(bwd) > 256
+    _run_case(w, opt=opt)
+
+
 def test_dw_accumulate():
     import paper_2510_04206_amd as P
     w = gen.make(gen.small_spec(V=600, d=128, dtype="bf16", name="acc"), seed=9)
@@ -166,7 +197,7 @@ def test_no_action_tokens_and_all_action_tokens():
     _run_case(w, adv=adv)
 
 
-def test_max_act_overflow_and_bad_token_flagged():
+def test_max_act_overflow_flagged():
     import paper_2510_04206_amd as P
     w = gen.make(gen.small_spec(V=400, d=64, dtype="bf16", name="flags"), seed=23)
     adv = torch.from_numpy(_adv(w)).cuda()
@@ -177,13 +208,51 @@ def test_max_act_overflow_and_bad_token_flagged():
                           d_in["old_logp"])
     assert np.isnan(loss.item())
     assert P.agrl_get_device_error() & 16
-    log("bad token id")
+    assert P.agrl_get_device_error() == 0
+
+
+# V = 400 is not a multiple of the 256-row tile: V pads the last vocabulary tile,
+# V_pad + 5 lies beyond it, -3 is negative
+@pytest.mark.parametrize("bad_id", [400, 517, -3])
+def test_bad_token_id_poisons_outputs(bad_id):
+    """An out-of-range id on an action token sets the error bit and turns that
+    token's logp / lse, the loss, its dH row and dW into NaN; every other token's
+    logp / lse is unchanged."""
+    import paper_2510_04206_amd as P
+    w = gen.make(gen.small_spec(V=400, d=64, dtype="bf16", name="bad ids"), seed=23)
+    adv = torch.from_numpy(_adv(w)).cuda()
+    d_in = to_dev(w)
+    log(f"bad token id {bad_id}")
     pl = P.PolicyLoss(w.T, w.d, w.V, w.H.dtype, max_act=w.n_act)
-    bad = d_in["token_id"].clone()
-    bad[int(np.nonzero(w.mask)[0][0])] = w.V
-    pl.forward(d_in["H"], d_in["W"], bad, d_in["mask"], adv, d_in["old_logp"])
+    good = run_gpu(pl, d_in, adv)
+    assert P.agrl_get_device_error() == 0
+    act = np.nonzero(w.mask)[0]
+    t_bad = int(act[len(act) // 2])
+    p_in = dict(d_in)
+    p_in["token_id"] = d_in["token_id"].clone()
+    p_in["token_id"][t_bad] = bad_id
+    g = run_gpu(pl, p_in, adv)
     assert P.agrl_get_device_error() & 1
     assert P.agrl_get_device_error() == 0
+    assert np.isnan(g["loss"])
+    assert np.isnan(g["logp"][t_bad]) and np.isnan(g["lse"][t_bad])
+    others = np.ones(w.T, bool)
+    others[t_bad] = False
+    np.testing.assert_array_equal(g["logp"][others], good["logp"][others])
+    np.testing.assert_array_equal(g["lse"][others], good["lse"][others])
+    assert np.isnan(g["dH"][t_bad]).all()
+    assert np.isnan(g["dW"]).all()
+    # masked rows of dH stay +0
+    off = w.mask == 0
+    assert np.all(g["dH"][off] == 0)
+    # the forward-only log-prob pass poisons the same token
+    lp = P.TokenLogprob(w.T, w.d, w.V, w.H.dtype, max_act=w.n_act)
+    logp, lse = lp(p_in["H"], p_in["W"], p_in["token_id"], p_in["mask"])
+    torch.cuda.synchronize()
+    assert P.agrl_get_device_error() & 1
+    logp, lse = logp.cpu().numpy(), lse.cpu().numpy()
+    assert np.isnan(logp[t_bad]) and np.isnan(lse[t_bad])
+    np.testing.assert_array_equal(logp[others], good["logp"][others].astype(np.float32))
 
 
 def test_argument_errors_on_gpu():
