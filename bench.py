@@ -173,7 +173,7 @@ def kernel_sources_digest() -> str:
 
 
 def committed_traffic(workload: str, kernel: str):
-    """HBM bytes per launch of `kernel` on `workload` from a committed counter summary.
+    """L2-to-fabric bytes per launch of `kernel` on `workload` from a committed counter summary.
 
     The summaries under profiles/ carry one line ``traffic-record: {json}`` with
     the sources digest they were measured on; a record whose digest differs from
@@ -191,13 +191,44 @@ def committed_traffic(workload: str, kernel: str):
     return None
 
 
+def host_cpu_info():
+    """What this process may run on: the host's logical CPUs, the CPUs in its
+    affinity mask, the cgroup CPU quota (cgroup v2 cpu.max, in CPUs; None when
+    unlimited or unreadable) and the CPU model from /proc/cpuinfo."""
+    info = {"host_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cgroup_cpu_quota": None, "cpu_model": None}
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            quota, period = f.read().split()[:2]
+        if quota != "max":
+            info["cgroup_cpu_quota"] = float(quota) / float(period)
+    except (OSError, ValueError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return info
+
+
 def cpu_baseline(w, adv_tok_host, n_sample, n_act, T):
-    """The oracle's fwd+bwd on the first n_sample action tokens, scaled to the micro-batch."""
+    """The oracle's fwd+bwd on the first n_sample action tokens, scaled to the micro-batch.
+
+    The oracle runs one thread per CPU this process may use: the affinity mask,
+    capped by the cgroup CPU quota when there is one (more threads than the
+    quota only time-slice)."""
     import oracle
     act = np.nonzero(w.mask)[0][:n_sample]
     H = w.H[torch.from_numpy(act).to(w.H.device)].cpu()
     W = w.W.cpu()
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    info = host_cpu_info()
+    threads = info["affinity_cpus"]
+    if info["cgroup_cpu_quota"]:
+        threads = min(threads, max(1, int(info["cgroup_cpu_quota"])))
     t0 = time.perf_counter()
     oracle.policy_loss(H, W, w.token_id[act], np.ones(len(act), np.uint8), adv_tok_host[act],
                        w.old_logp[act], eps_lo=w.spec.eps_lo, eps_hi=w.spec.eps_hi,
@@ -209,7 +240,7 @@ def cpu_baseline(w, adv_tok_host, n_sample, n_act, T):
             "sample": f"fwd+bwd (logp, loss, dH, dW) of {len(act)} of the micro-batch's {n_act} "
                       f"action tokens over the full V={w.V}, d={w.d} in fp64 took {dt:.2f} s on "
                       f"{threads} threads; value = T / (time per action token * N_act)",
-            "seconds": dt}
+            "seconds": dt, **info}
 
 
 def main():
@@ -222,7 +253,7 @@ def main():
                     help="action tokens in the oracle's timed sample (0 skips it)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before the steps, copy a buffer of this many MiB once (a kernel of known "
-                         "traffic, to scale the HBM counters of a profiling run)")
+                         "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path; "
@@ -393,8 +424,10 @@ def main():
                      "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": rec["bytes_per_launch"] if rec else None,
-                     "traffic_unit": "bytes per launch (HBM reads + writes, rocprofv3 FETCH_SIZE "
-                                     "and WRITE_SIZE scaled by a copy kernel of known size)",
+                     "traffic_unit": "bytes per launch between the L2 caches and the fabric "
+                                     "(reads + writes; Infinity Cache hits included, so an upper "
+                                     "bound on HBM traffic): rocprofv3 FETCH_SIZE and WRITE_SIZE "
+                                     "scaled by a copy kernel of known size",
                      "flops_per_launch": per_launch[dom]},
         "sclk_mhz": sclk,
         "board_power_w": board_power,
