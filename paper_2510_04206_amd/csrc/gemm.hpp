@@ -73,6 +73,9 @@ struct GemmShape {
   // of a column-block tiled matrix whose rows are the product's K and whose
   // columns are the product's rows (lda = its padded row count).
   int32_t a_tiled, b_tiled, a_trans;
+  // bf16 kernel only: 1 makes the tile-order groups run over column tiles
+  // (group_m column tiles deep, sweeping every row tile) instead of row tiles
+  int32_t group_cols;
 };
 
 // Stage-tiled bf16 layout of a matrix with rows r and K-columns k (K padded to
@@ -491,7 +494,10 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     const int nk = (p ? Kp[1] : Kp[0]) / SK;
     int tm, tn;
     const int L = p ? queue_tile(t - sh[0].len, sh[1], qi, nq) : queue_tile(t, sh[0], qi, nq);
-    grouped_tile(L, p ? tmp[1] : tmp[0], p ? tnp[1] : tnp[0], g.group_m, tm, tn);
+    if (g.group_cols)
+      grouped_tile(L, p ? tnp[1] : tnp[0], p ? tmp[1] : tmp[0], g.group_m, tn, tm);
+    else
+      grouped_tile(L, p ? tmp[1] : tmp[0], p ? tnp[1] : tnp[0], g.group_m, tm, tn);
     const int64_t lda_b = g.lda * 2, ldb_b = g.ldb * 2;
     const int m0 = tm * GBM, n0 = tn * GBN;
     const bool atr = ATR && g.a_trans;

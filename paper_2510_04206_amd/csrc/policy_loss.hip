@@ -803,7 +803,11 @@ void bwd_gemms(const Common& c, const Layout& L, uint8_t* ws, const void* W, flo
       g.m_dev = ctrl;
       g.N = nv;
       g.K = c.d;
+      // groups of 8 vocabulary tiles sweep every token tile: each W panel of the
+      // chunk is read from memory once (the compacted H is small enough to stay
+      // in the Infinity Cache), not once per group of 8 token tiles
       g.group_m = 8;
+      g.group_cols = 1;
       EpiLogitGrad<T> e;
       e.y = (const int32_t*)(ws + L.y_act);
       e.lse = (const float*)(ws + L.lse_act);
