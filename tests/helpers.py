@@ -54,8 +54,16 @@ def near_clip(logp, old, adv, mask, eps_lo, eps_hi, tol=1e-4):
     return m & (hi | lo)
 
 
-def compare_loss(gpu, ref, w_mask, adv, old, eps_lo, eps_hi, *, loss_rel=1e-3, lp_atol=2e-3,
-                 grad_rel=2e-2, check_grads=True):
+# lse / logp, absolute: about 5x the largest error measured over every parity case
+# (full-size workloads included: 1.8e-6 for lse, 8.5e-6 for logp at d = 5120),
+# which follows from fp32 accumulation of bf16 products over d terms (~sqrt(d)
+# roundings of 2^-24 relative on logits of magnitude ~1)
+LSE_ATOL = 2e-5
+LOGP_ATOL = 5e-5
+
+
+def compare_loss(gpu, ref, w_mask, adv, old, eps_lo, eps_hi, *, loss_rel=1e-3, lp_atol=LOGP_ATOL,
+                 lse_atol=LSE_ATOL, grad_rel=2e-2, check_grads=True):
     """Element-by-element comparison of one fwd(+bwd) against the oracle's whole batch."""
     m = np.asarray(w_mask).astype(bool)
     logp = gpu["logp"]
@@ -66,10 +74,10 @@ def compare_loss(gpu, ref, w_mask, adv, old, eps_lo, eps_hi, *, loss_rel=1e-3, l
     if m.any():
         e_lse = float(np.abs(lse[m] - ref["lse"][m]).max())
         e_lp = float(np.abs(logp[m] - ref["logp"][m]).max())
-        log(f"  max |d lse| {e_lse:.3e}  max |d logp| {e_lp:.3e}  (atol {lp_atol:.1e}); "
-            f"loss rel err {abs(L - R) / max(abs(R), 1e-30):.3e}")
-    np.testing.assert_allclose(lse[m], ref["lse"][m], rtol=1e-5, atol=lp_atol)
-    np.testing.assert_allclose(logp[m], ref["logp"][m], rtol=1e-5, atol=lp_atol)
+        log(f"  max |d lse| {e_lse:.3e} (atol {lse_atol:.0e})  max |d logp| {e_lp:.3e} "
+            f"(atol {lp_atol:.0e}); loss rel err {abs(L - R) / max(abs(R), 1e-30):.3e}")
+    np.testing.assert_allclose(lse[m], ref["lse"][m], rtol=0, atol=lse_atol)
+    np.testing.assert_allclose(logp[m], ref["logp"][m], rtol=0, atol=lp_atol)
     assert abs(L - R) <= loss_rel * abs(R) + 1e-7, (L, R)
     flips = near_clip(ref["logp"], old, adv, m, eps_lo, eps_hi)
     assert np.abs(np.asarray(gpu["n_clip"]) - ref["n_clip"]).sum() <= flips.sum()

@@ -3,8 +3,8 @@
 Against the oracle (log-softmax of the logits at the sampled ids, fp64) on
 small workloads with ragged tiles, and bit-for-bit against the policy-loss
 forward on the same inputs (same tiles, partials and merge), also at the
-32B-shaped size.  Tolerance: 2e-3 absolute (+1e-5 relative), as for the
-forward's logp: z is an fp32 sum of exact bf16 products over d terms.
+32B-shaped size.  Tolerances as for the forward's lse and logp (helpers.LSE_ATOL,
+LOGP_ATOL): z is an fp32 sum of exact bf16 products over d terms.
 """
 import numpy as np
 import pytest
@@ -13,7 +13,7 @@ import torch
 import oracle
 from workloads import gen
 
-from helpers import log, to_dev
+from helpers import LOGP_ATOL, LSE_ATOL, log, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -45,8 +45,8 @@ def test_logprob_against_oracle(name, kw):
     r = oracle.token_logprob(w.H, w.W, w.token_id, w.mask)
     m = w.mask.astype(bool)
     assert np.all(logp[~m] == 0) and np.all(lse[~m] == 0)
-    np.testing.assert_allclose(lse[m], r["lse"][m], rtol=1e-5, atol=2e-3)
-    np.testing.assert_allclose(logp[m], r["logp"][m], rtol=1e-5, atol=2e-3)
+    np.testing.assert_allclose(lse[m], r["lse"][m], rtol=0, atol=LSE_ATOL)
+    np.testing.assert_allclose(logp[m], r["logp"][m], rtol=0, atol=LOGP_ATOL)
 
 
 def test_logprob_temperature():
@@ -55,7 +55,7 @@ def test_logprob_temperature():
     logp, lse = _logprob(w, to_dev(w), opt={"temperature": 0.8})
     r = oracle.token_logprob(w.H, w.W, w.token_id, w.mask, temperature=0.8)
     m = w.mask.astype(bool)
-    np.testing.assert_allclose(logp[m], r["logp"][m], rtol=1e-5, atol=2e-3)
+    np.testing.assert_allclose(logp[m], r["logp"][m], rtol=0, atol=LOGP_ATOL)
 
 
 def test_logprob_no_action_tokens_and_empty():

@@ -4,7 +4,7 @@ The KL term (App. A objectives, -beta D_KL; k3 and k1 estimators) and the
 per-token weights (sequence-level aggregation of App. B.2's GRPO form, a
 token mean per trajectory then a mean over trajectories) change only the
 per-token loss and dL/dlogp; the same tolerances as the plain loss apply:
-loss 1e-3 relative, logp 2e-3 absolute, dH/dW 2e-2 relative Frobenius.
+loss 1e-3 relative, lse 2e-5 and logp 5e-5 absolute, dH/dW 2e-2 relative Frobenius.
 """
 import numpy as np
 import pytest
