@@ -266,6 +266,29 @@ int agrl_token_logprob(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t
                        const uint8_t* action_mask, const agrl_options* opt, void* workspace,
                        size_t ws_bytes, float* logp, float* lse, void* stream);
 
+/*
+ * agrl_token_logprob without a workspace argument, for callers that cannot
+ * allocate device memory around the call: code being captured into a HIP
+ * graph, tight serving loops, harnesses that forbid allocation.  The same
+ * kernels, outputs and errors as agrl_token_logprob; their workspace is a
+ * fixed array of AGRL_NOALLOC_SCRATCH_BYTES of device memory that the library
+ * holds on every GPU it runs on until the process ends.  The call allocates
+ * nothing (no hipMalloc, no library routine that allocates); the caller still
+ * passes the inputs and outputs.
+ *   Arguments as for agrl_token_logprob, without workspace and ws_bytes.
+ *   Sizes whose agrl_token_logprob_workspace_size exceeds the array are
+ *   refused with AGRL_E_WORKSPACE before anything is launched.
+ * Every call on one GPU uses that GPU's array, and an array keeps what the
+ * last call left in it (nothing in it needs to start at zero: the kernels
+ * write every value they read).  Calls that overlap on one GPU, from two
+ * streams or two host threads, race on the array; serialise them.
+ */
+#define AGRL_NOALLOC_SCRATCH_BYTES (64ll << 20)
+int agrl_token_logprob_noalloc(int64_t T, int64_t max_act, int32_t d, int32_t V, int32_t dtype,
+                               const void* H, const void* W, const int32_t* token_id,
+                               const uint8_t* action_mask, const agrl_options* opt, float* logp,
+                               float* lse, void* stream);
+
 /* Text for a status code (static storage). */
 const char* agrl_status_string(int status);
 

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libagrl.so")
 
 AGRL_BF16 = 0
 AGRL_F32 = 1
+AGRL_NOALLOC_SCRATCH_BYTES = 64 << 20     # include/agrl.h
 ERROR_BITS = {1: "token id out of range", 2: "trajectory id out of range",
               4: "task id out of range", 8: "group id out of range",
               16: "more action tokens than max_act"}
@@ -57,6 +58,8 @@ _SIGS = {
     "agrl_token_logprob_workspace_size": (_c_sz, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
     "agrl_token_logprob": (_c_i32, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p,
                                     _c_p, _c_p, _c_sz, _c_p, _c_p, _c_p]),
+    "agrl_token_logprob_noalloc": (_c_i32, [_c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p,
+                                            _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "agrl_sequence_mean_weights": (_c_i32, [_c_i64, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "agrl_status_string": (ctypes.c_char_p, [_c_i32]),
     "agrl_last_error": (ctypes.c_char_p, []),
@@ -169,6 +172,13 @@ def agrl_token_logprob(T, max_act, d, V, dtype, H, W, token_id, action_mask, opt
     _check("agrl_token_logprob", lib().agrl_token_logprob(
         T, max_act, d, V, dtype, _ptr(H), _ptr(W), _ptr(token_id), _ptr(action_mask), _opts(opt),
         _ptr(workspace), ws_bytes, _ptr(logp), _ptr(lse), _stream(stream)))
+
+
+def agrl_token_logprob_noalloc(T, max_act, d, V, dtype, H, W, token_id, action_mask, opt, logp,
+                               lse, stream=None) -> None:
+    _check("agrl_token_logprob_noalloc", lib().agrl_token_logprob_noalloc(
+        T, max_act, d, V, dtype, _ptr(H), _ptr(W), _ptr(token_id), _ptr(action_mask), _opts(opt),
+        _ptr(logp), _ptr(lse), _stream(stream)))
 
 
 def agrl_sequence_mean_weights(T, n_traj, traj_id, action_mask, seq_count, token_weight,

@@ -10,7 +10,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libagrl.so")
-SOURCES = ["abi.hip", "adv_norm.hip", "policy_loss.hip"]
+SOURCES = ["abi.hip", "adv_norm.hip", "policy_loss.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
