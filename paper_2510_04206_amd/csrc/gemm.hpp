@@ -4,7 +4,10 @@
 //
 // Block tile 256 x 256, 4 waves in a 2 x 2 arrangement, each wave owning a
 // 128 x 128 sub-tile as 4 x 4 blocks of 32 x 32 MFMA accumulators
-// (v_mfma_f32_32x32x16_bf16 for bf16, v_mfma_f32_32x32x2_f32 for fp32).
+// (v_mfma_f32_32x32x16_bf16 for bf16, v_mfma_f32_32x32x2_f32 for fp32), or, in
+// the bf16 kernel's 16 x 16 mode, as 8 x 8 blocks of v_mfma_f32_16x16x32_bf16
+// accumulators (half the accumulator traffic per flop: under the board power
+// limit the chip then holds a higher clock).
 // Each K stage moves 128 bytes of every tile row (64 bf16 or 32 fp32) from
 // global memory straight into LDS (no register staging), double-buffered with
 // one barrier per stage.  The 16-byte chunk c of tile row r is stored at chunk
@@ -21,6 +24,7 @@
 // the 32 workgroups of an XCD share A and B panels in its L2.
 #pragma once
 #include <type_traits>
+#include <utility>
 
 #include "common.hpp"
 
@@ -356,6 +360,36 @@ __device__ __forceinline__ void copy16(const void* base, uint32_t off, uint32_t 
                : "memory");
 }
 
+// 16 x 16 x 32 loop: what rides along with MFMA slot q of a stage (slot
+// q = 16 i + 2 j + kk is block (i, j), slice kk).  Copy c of the stage after
+// next in slot CS c (spread out: a burst of copies stalls issue when the
+// memory pipeline is backed up, and the wave's matrix pipe waits with it; the
+// later a copy, the less time it has to land before the next stage starts);
+// the next stage's A rows i < 7 in place, two slots after row i's last MFMA;
+// its row 7 (into the spare set) and its B fragments in the remaining odd
+// slots below 64, so every read has half a stage or more before its first use.
+constexpr int MF16_NONE = -1, MF16_COPY = 0, MF16_BREAD = 16, MF16_AREAD = 32;
+__device__ __forceinline__ constexpr bool mf16_arow_slot(int q) {
+  return (q & 1) == 1 && q >= 17 && (q - 17) % 16 < 4 && (q - 17) / 16 < 7;
+}
+// CS: slots between two copies (even, so that copies never share a slot with
+// a fragment read)
+template <int CS>
+__device__ __forceinline__ constexpr int mf16_slot(int q) {
+  static_assert(CS % 2 == 0 && 15 * CS < 128, "copy spacing");
+  if (q < 16 * CS && q % CS == 0) return MF16_COPY + q / CS;
+  if (mf16_arow_slot(q)) return MF16_AREAD + 2 * ((q - 17) / 16) + ((q - 17) % 16) / 2;
+  if (q == 41 || q == 43) return MF16_AREAD + 14 + (q - 41) / 2;
+  if ((q & 1) == 1 && q < 64) {
+    // the n-th odd slot below 64 not taken above carries B read n
+    int n = 0;
+    for (int p = 1; p < q; p += 2)
+      if (!mf16_arow_slot(p) && p != 41 && p != 43) ++n;
+    return n < 16 ? MF16_BREAD + n : MF16_NONE;
+  }
+  return MF16_NONE;
+}
+
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 __device__ __forceinline__ bf16x4 read_tr(const uint8_t* p) {
@@ -363,6 +397,16 @@ __device__ __forceinline__ bf16x4 read_tr(const uint8_t* p) {
 }
 
 }  // namespace bf16k
+
+// f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N - 1>{})
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // The lane index computed afresh (from the exec mask, not from threadIdx.x), so
 // that quantities derived from it are formed where they are used instead of
@@ -386,6 +430,21 @@ struct GemmBatch {
   Epi e[2];
   int32_t n;          // number of problems
   int32_t* queue;     // 8 tile counters, zero at launch
+};
+
+// Copy schedule of the 16 x 16 loop, per epilogue (measured on the 32B-shaped
+// workload): MFMA slots between two stage copies, and whether A's copies go
+// before B's.
+template <class Epi>
+struct CopySched {
+  static constexpr int spacing = 4;
+  static constexpr bool a_first = false;
+};
+struct EpiLseCols;
+template <>
+struct CopySched<EpiLseCols> {
+  static constexpr int spacing = 6;
+  static constexpr bool a_first = false;
 };
 
 // Tile scheduling.  Workgroups are dealt round-robin to the 8 XCDs, so
@@ -434,10 +493,11 @@ __device__ __forceinline__ int queue_tile(int k, const QueueShare& s, int q, int
 // unrolled by two and each stage knows its buffer at compile time, so every LDS
 // address of the loop is a base register plus an immediate.  ATR: a problem may
 // read A transposed (GemmShape::a_trans; EVEN launches only).
-template <class Epi, bool EVEN, bool ATR>
+template <class Epi, bool EVEN, bool ATR, bool MF16 = false>
 __global__ void __launch_bounds__(GEMM_THREADS)
     __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmBatch<Epi> bat) {
   static_assert(EVEN || !ATR, "transposed A in the stage-pair loop only");
+  static_assert(!MF16 || EVEN, "the 16 x 16 loop runs stage pairs");
   using namespace bf16k;
   __shared__ __attribute__((aligned(16))) uint8_t smem[BF16_KERNEL_LDS];
   __shared__ int s_tile;
@@ -557,9 +617,13 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         const int kr = wave * 16 + 2 * b + (ln >> 5);
         const int p = ln & 31;
         const int w = (p >> 2) ^ (kr & 3);
+        // 16 x 16 loop: the 32-byte halves of a window are swapped when bit 3 of
+        // the k-row is set, so lane i holds rows 32 w + 16 hf + 8 (i & 1) .. + 7
+        const int c16 = MF16 ? (w & 1) * 4 + ((((p >> 1) & 1) ^ ((kr >> 3) & 1)) << 1) + (p & 1)
+                             : (w & 1) * 4 + (p & 3);
         // (lda <= 2^23 rows: at most 3 * 2^15 blocks of 32 KiB, within 32 bits)
         offa[b] = (uint32_t)((w >> 1) * (uint32_t)((g.lda >> 8) * HALF) + kr * ROW +
-                             ((((w & 1) * 4 + (p & 3)) ^ ((kr >> 1) & 7)) << 4));
+                             ((c16 ^ ((kr >> 1) & 7)) << 4));
       }
     }
 
@@ -603,144 +667,293 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     };
     using BUF_RT = std::integral_constant<int, -1>;
 
-    f32x16 acc[4][4];
+    if constexpr (MF16) {
+      // 16 x 16 x 32 loop.  acc[i][j] is the 16 x 16 block (i, j) of the wave's
+      // 128 x 128 sub-tile: lane l holds column 16 j + (l & 15), rows 16 i +
+      // 4 (l >> 4) .. + 3.  A stage is two 32-deep slices; the MFMAs of a stage
+      // run rows i = 0..7, columns j = 0..7, and the two slices of block (i, j)
+      // back to back (the second accumulates onto the first).  The stage's
+      // fragments are in registers before it starts: fa[i][kk] (A, replaced in
+      // place by the next stage's row i once row i's MFMAs are issued; row 7 of
+      // odd stages lives in fa7) and fb[P][j][kk] (B, two sets by stage parity).
+      // One barrier per stage, at its start: the next stage has landed and
+      // every wave is done reading this stage's buffer, which the copies of
+      // the stage after next then refill.
+      // one accumulator set and one epilogue for both operand modes (TR: A
+      // read transposed); only the main loop is instantiated per mode
+      f32x4 acc[8][8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      auto loop16 = [&](auto tr_c) {
+      constexpr bool TR = decltype(tr_c)::value;
+      {
+        // lane l reads row l & 15 of each 16-row block, 16-byte chunk
+        // 4 kk + (l >> 4) of slice kk; the row swizzle depends on the row within
+        // the block only, so a block is an immediate offset of 2 KiB.
+        // Transposed A: the stage's A half holds 64 k-rows of 512 bytes; the
+        // 64-byte window w (rows 32 w .. + 31) of k-row k sits at w ^ (k & 3)
+        // and its 32-byte halves are swapped when bit 3 of k is set.  Block i
+        // of slice kk is two transposing reads (ds_read_b64_tr_b16): in 16-lane
+        // group g, lane s supplies k-row 32 kk + 8 g + (s >> 2) (+ 4 for the
+        // second read) and rows 4 (s & 3) .. + 3 of the block, and lane s
+        // receives row s of those 4 k-rows.  A 32-lane half touches 8 k-rows,
+        // spread over 4 bank windows by (k & 3) and 2 halves by bit 3 of k.
+        const int l16 = fresh_lane();
+        const int fr = l16 & 15;
+        int ra16[2], rb16[2];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-    if (nk > 0) {
-      // stage 0 whole; stage 1's slot 0..15 copies (stage 0 issues the rest)
-#pragma unroll
-      for (int q = 0; q < NCOPY; ++q) copy_q(0, q, std::integral_constant<int, 0>{}, 0);
-      if (nk > 1) {
-#pragma unroll
-        for (int c = 0; c < NEARLY; ++c)
-          copy_q(1, copy_order(c), std::integral_constant<int, 1>{}, 1);
-        wait_vmcnt<NEARLY>();      // stage 0 landed
-      } else {
-        wait_vmcnt<0>();
-      }
-      __builtin_amdgcn_s_barrier();
-      // TR: A is read transposed (two half-fragment reads per 32-row block)
-      auto pipeline = [&](auto tr_c) {
-        constexpr bool TR = decltype(tr_c)::value;
-        // transposed A: lane l supplies k-row 8 (l >> 5) + ((l >> 2) & 3) of the
-        // slice and rows 16 ((l >> 4) & 1) + 4 (l & 3) .. + 3 of 32-block i
-        int ta[4];
+        for (int kk = 0; kk < 2; ++kk) {
+          const int chk = ((kk * 4 + (l16 >> 4)) ^ row_swizzle(fr)) << 4;
+          ra16[kk] = (wm * 128 + fr) * ROW + chk;
+          rb16[kk] = NB * HALF + (wn * 128 + fr) * ROW + chk;
+        }
+        // block i's transposed read: ta16 ^ (64 (i >> 1) + 32 (i & 1)) (the
+        // window and half bits of ta16 hold the lane's XOR pattern; the block's
+        // bits go in by one XOR per read instead of eight live addresses)
+        int ta16 = 0;
         if constexpr (TR) {
-          const int l = fresh_lane();
-          const int q4 = (l >> 2) & 3;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            ta[i] = (8 * (l >> 5) + q4) * TR_KROW + (4 * wm + (i ^ q4)) * 64 +
-                    32 * ((l >> 4) & 1) + 8 * (l & 3);
+          const int g = l16 >> 4, q4 = (l16 >> 2) & 3;
+          ta16 = (8 * g + q4) * TR_KROW + 4 * wm * 64 + (q4 << 6) + ((g & 1) << 5) + 8 * (l16 & 3);
         }
-        // the fragment read paired with MFMA q of a slice (slice kn, buffer
-        // offset off): A blocks first (two halves each when transposed), then B
-        auto frag = [&](int q, int kn, int off, bf16x8 (&fan)[4], bf16x8 (&fbn)[4]) {
+        auto rd_a = [&](int i, int kk, int buf) {
           if constexpr (TR) {
-            if (q < 8) {
-              const int i = q >> 1;
-              if (q & 1)
-                fan[i].hi = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW + 4 * TR_KROW);
-              else
-                fan[i].lo = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW);
-            } else if (q < 12) {
-              fbn[q - 8] = *(const bf16x8*)(smem + rb[kn] + off + (q - 8) * 32 * ROW);
-            }
+            const uint8_t* p = smem + (ta16 ^ ((i >> 1) << 6 | (i & 1) << 5)) + buf * HALF +
+                               kk * 32 * TR_KROW;
+            bf16x8 v;
+            v.lo = read_tr(p);
+            v.hi = read_tr(p + 4 * TR_KROW);
+            return v;
           } else {
-            if (q < 4)
-              fan[q] = *(const bf16x8*)(smem + ra[kn] + off + q * 32 * ROW);
-            else if (q < 8)
-              fbn[q - 4] = *(const bf16x8*)(smem + rb[kn] + off + (q - 4) * 32 * ROW);
+            return *(const bf16x8*)(smem + ra16[kk] + buf * HALF + i * 16 * ROW);
           }
         };
-        bf16x8 fa[2][4], fb[2][4];
+        auto rd_b = [&](int j, int kk, int buf) {
+          return *(const bf16x8*)(smem + rb16[kk] + buf * HALF + j * 16 * ROW);
+        };
+        // stages 0 and 1 whole
 #pragma unroll
-        for (int q = 0; q < 16; ++q) frag(q, 0, 0, fa[0], fb[0]);
-
-        // P: stage kt's buffer (kt % NB), known at compile time when >= 0
-        auto stage = [&](int kt, auto refill_c, auto more_c, auto par_c) {
-          constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
-          constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
-          constexpr int P = decltype(par_c)::value;
+        for (int q = 0; q < NCOPY; ++q) copy_q(0, q, std::integral_constant<int, 0>{}, 0);
+#pragma unroll
+        for (int q = 0; q < NCOPY; ++q) copy_q(1, q, std::integral_constant<int, 1>{}, 1);
+        wait_vmcnt<NCOPY>();        // stage 0 landed (stage pairs: nk >= 2)
+        __builtin_amdgcn_s_barrier();
+        using P0 = std::integral_constant<int, 0>;
+        using P1 = std::integral_constant<int, 1>;
+        // stage 0's fragments
+        bf16x8 fa[8][2], fa7[2], fb[2][8][2];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            fa[i][kk] = rd_a(i, kk, 0);
+            fb[0][i][kk] = rd_b(i, kk, 0);
+          }
+        // Every stage runs the same code (one register assignment for the whole
+        // loop): the last two stages copy the last stage again into the buffer
+        // they free (its data is in registers already, nothing reads it again),
+        // and the last stage reads stale fragments of a stage that does not
+        // exist; both stay within the operands and the LDS.
+        auto stage16 = [&](int kt, auto par_c) {
+          constexpr int P = decltype(par_c)::value;            // kt % 2
           using PC = std::integral_constant<int, P>;
-          using PN = std::integral_constant<int, P >= 0 ? (P ^ 1) : -1>;
-          const int pr = P >= 0 ? P : (kt % NB);               // this stage's buffer
-          const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
+          const int kc = min(kt + 2, nk - 1);                  // stage to copy
+          wait_vmcnt<0>();                                     // stage kt + 1 landed
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage kt's fragments
+          __builtin_amdgcn_s_barrier();
           __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-          for (int kk = 0; kk < KK; ++kk) {
-            const int cur = kk & 1, nxt = cur ^ 1;
-            if (kk == KK - 1) {
-              if constexpr (MORE) {
-                // stage kt+1 landed (its copies are the only ones in flight)
-                wait_vmcnt<0>();
-              }
-              asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-              __builtin_amdgcn_s_barrier();
-              __builtin_amdgcn_sched_barrier(0);
-            }
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-              const int i = q >> 2, j = q & 3;
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
+          // (every index below is a compile-time constant, so that the
+          // fragment and accumulator arrays stay in registers)
+          static_for<128>([&](auto q_c) {
+            constexpr int q = decltype(q_c)::value;
+            constexpr int i = q >> 4, j = (q >> 1) & 7, kk = q & 1;
+            constexpr int op = mf16_slot<CopySched<Epi>::spacing>(q);
+            if constexpr (i == 7 && P == 1)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa7[kk], fb[P][j][kk], acc[i][j],
                                                                   0, 0, 0);
-              if (kk < KK - 1) {
-                frag(q, kk + 1, cur_off, fa[nxt], fb[nxt]);
-                if constexpr (MORE) {
-                  const int slot = 16 * (kk + 1) + q;
-                  if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
-                    copy_q(kt + 1, copy_order(slot / CSTRIDE), PN{}, pr ^ 1);
-                }
-              } else {
-                if constexpr (MORE) frag(q, 0, nxt_off, fa[nxt], fb[nxt]);
-                if constexpr (REFILL) {
-                  if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), PC{}, pr);
-                }
-              }
-              __builtin_amdgcn_sched_barrier(0);
+            else
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i][kk], fb[P][j][kk],
+                                                                  acc[i][j], 0, 0, 0);
+            if constexpr (op >= MF16_COPY && op < MF16_COPY + 16) {
+              constexpr int c = op - MF16_COPY;
+              copy_q(kc, CopySched<Epi>::a_first ? c : copy_order(c), PC{}, P);
+            } else if constexpr (op >= MF16_BREAD && op < MF16_BREAD + 16) {
+              constexpr int n = op - MF16_BREAD;
+              fb[P ^ 1][n >> 1][n & 1] = rd_b(n >> 1, n & 1, P ^ 1);
+            } else if constexpr (op >= MF16_AREAD && op < MF16_AREAD + 16) {
+              constexpr int n = op - MF16_AREAD, ia = n >> 1, ka = n & 1;
+              // the next stage's row 7 goes to the set this stage does not use
+              if constexpr (ia == 7 && P == 0)
+                fa7[ka] = rd_a(7, ka, P ^ 1);
+              else
+                fa[ia][ka] = rd_a(ia, ka, P ^ 1);
             }
+            __builtin_amdgcn_sched_barrier(0);
+          });
+        };
+        for (int kt = 0; kt < nk; kt += 2) {
+          stage16(kt, P0{});
+          stage16(kt + 1, P1{});
+        }
+      }
+      };
+      if (nk > 0) {
+        if constexpr (ATR) {
+          if (atr)
+            loop16(std::true_type{});
+          else
+            loop16(std::false_type{});
+        } else {
+          loop16(std::false_type{});
+        }
+      }
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+      {
+        const int lane_e = fresh_lane();
+        epi.tile16(acc, m0, n0, tn, M, N, smem, wm, wn, lane_e, wave * 64 + lane_e);
+      }
+    } else {
+      f32x16 acc[4][4];
+  #pragma unroll
+      for (int i = 0; i < 4; ++i)
+  #pragma unroll
+        for (int j = 0; j < 4; ++j)
+  #pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+      if (nk > 0) {
+        // stage 0 whole; stage 1's slot 0..15 copies (stage 0 issues the rest)
+  #pragma unroll
+        for (int q = 0; q < NCOPY; ++q) copy_q(0, q, std::integral_constant<int, 0>{}, 0);
+        if (nk > 1) {
+  #pragma unroll
+          for (int c = 0; c < NEARLY; ++c)
+            copy_q(1, copy_order(c), std::integral_constant<int, 1>{}, 1);
+          wait_vmcnt<NEARLY>();      // stage 0 landed
+        } else {
+          wait_vmcnt<0>();
+        }
+        __builtin_amdgcn_s_barrier();
+        // TR: A is read transposed (two half-fragment reads per 32-row block)
+        auto pipeline = [&](auto tr_c) {
+          constexpr bool TR = decltype(tr_c)::value;
+          // transposed A: lane l supplies k-row 8 (l >> 5) + ((l >> 2) & 3) of the
+          // slice and rows 16 ((l >> 4) & 1) + 4 (l & 3) .. + 3 of 32-block i
+          int ta[4];
+          if constexpr (TR) {
+            const int l = fresh_lane();
+            const int q4 = (l >> 2) & 3;
+  #pragma unroll
+            for (int i = 0; i < 4; ++i)
+              ta[i] = (8 * (l >> 5) + q4) * TR_KROW + (4 * wm + (i ^ q4)) * 64 +
+                      32 * ((l >> 4) & 1) + 8 * (l & 3);
+          }
+          // the fragment read paired with MFMA q of a slice (slice kn, buffer
+          // offset off): A blocks first (two halves each when transposed), then B
+          auto frag = [&](int q, int kn, int off, bf16x8 (&fan)[4], bf16x8 (&fbn)[4]) {
+            if constexpr (TR) {
+              if (q < 8) {
+                const int i = q >> 1;
+                if (q & 1)
+                  fan[i].hi = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW + 4 * TR_KROW);
+                else
+                  fan[i].lo = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW);
+              } else if (q < 12) {
+                fbn[q - 8] = *(const bf16x8*)(smem + rb[kn] + off + (q - 8) * 32 * ROW);
+              }
+            } else {
+              if (q < 4)
+                fan[q] = *(const bf16x8*)(smem + ra[kn] + off + q * 32 * ROW);
+              else if (q < 8)
+                fbn[q - 4] = *(const bf16x8*)(smem + rb[kn] + off + (q - 4) * 32 * ROW);
+            }
+          };
+          bf16x8 fa[2][4], fb[2][4];
+  #pragma unroll
+          for (int q = 0; q < 16; ++q) frag(q, 0, 0, fa[0], fb[0]);
+
+          // P: stage kt's buffer (kt % NB), known at compile time when >= 0
+          auto stage = [&](int kt, auto refill_c, auto more_c, auto par_c) {
+            constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
+            constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
+            constexpr int P = decltype(par_c)::value;
+            using PC = std::integral_constant<int, P>;
+            using PN = std::integral_constant<int, P >= 0 ? (P ^ 1) : -1>;
+            const int pr = P >= 0 ? P : (kt % NB);               // this stage's buffer
+            const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
+            __builtin_amdgcn_sched_barrier(0);
+  #pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+              const int cur = kk & 1, nxt = cur ^ 1;
+              if (kk == KK - 1) {
+                if constexpr (MORE) {
+                  // stage kt+1 landed (its copies are the only ones in flight)
+                  wait_vmcnt<0>();
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+              }
+  #pragma unroll
+              for (int q = 0; q < 16; ++q) {
+                const int i = q >> 2, j = q & 3;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
+                                                                    0, 0, 0);
+                if (kk < KK - 1) {
+                  frag(q, kk + 1, cur_off, fa[nxt], fb[nxt]);
+                  if constexpr (MORE) {
+                    const int slot = 16 * (kk + 1) + q;
+                    if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
+                      copy_q(kt + 1, copy_order(slot / CSTRIDE), PN{}, pr ^ 1);
+                  }
+                } else {
+                  if constexpr (MORE) frag(q, 0, nxt_off, fa[nxt], fb[nxt]);
+                  if constexpr (REFILL) {
+                    if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), PC{}, pr);
+                  }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            }
+          };
+          using T_ = std::true_type;
+          using F_ = std::false_type;
+          if constexpr (EVEN) {
+            // nk even: pairs of stages with buffers 0 and 1, the last pair without
+            // copies of further stages
+            using P0 = std::integral_constant<int, 0>;
+            using P1 = std::integral_constant<int, 1>;
+            int kt = 0;
+            for (; kt + NB < nk; kt += 2) {
+              stage(kt, T_{}, T_{}, P0{});
+              stage(kt + 1, T_{}, T_{}, P1{});
+            }
+            stage(kt, F_{}, T_{}, P0{});
+            stage(kt + 1, F_{}, F_{}, P1{});
+          } else {
+            int kt = 0;
+            for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{}, BUF_RT{});
+            for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{}, BUF_RT{});
+            stage(kt, F_{}, F_{}, BUF_RT{});
           }
         };
-        using T_ = std::true_type;
-        using F_ = std::false_type;
-        if constexpr (EVEN) {
-          // nk even: pairs of stages with buffers 0 and 1, the last pair without
-          // copies of further stages
-          using P0 = std::integral_constant<int, 0>;
-          using P1 = std::integral_constant<int, 1>;
-          int kt = 0;
-          for (; kt + NB < nk; kt += 2) {
-            stage(kt, T_{}, T_{}, P0{});
-            stage(kt + 1, T_{}, T_{}, P1{});
-          }
-          stage(kt, F_{}, T_{}, P0{});
-          stage(kt + 1, F_{}, F_{}, P1{});
+        if constexpr (ATR) {
+          if (atr)
+            pipeline(std::true_type{});
+          else
+            pipeline(std::false_type{});
         } else {
-          int kt = 0;
-          for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{}, BUF_RT{});
-          for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{}, BUF_RT{});
-          stage(kt, F_{}, F_{}, BUF_RT{});
-        }
-      };
-      if constexpr (ATR) {
-        if (atr)
-          pipeline(std::true_type{});
-        else
           pipeline(std::false_type{});
-      } else {
-        pipeline(std::false_type{});
+        }
       }
-    }
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-    __syncthreads();
-    {
-      const int lane_e = fresh_lane();
-      epi.tile(acc, m0, n0, tn, M, N, smem, wm, wn, lane_e, wave * 64 + lane_e);
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+      {
+        const int lane_e = fresh_lane();
+        epi.tile(acc, m0, n0, tn, M, N, smem, wm, wn, lane_e, wave * 64 + lane_e);
+      }
     }
     __syncthreads();
   }
@@ -991,6 +1204,90 @@ struct EpiLseCols {
       part[(int64_t)(m0 / GBM) * ld_part + col] = f32x2{m, s};
     }
   }
+
+  // The same on the 16 x 16 accumulator layout: lane l holds 8 token columns
+  // (16 j + (l & 15)) and 32 vocabulary rows of each (16 i + 4 (l >> 4) + r),
+  // the other 96 rows of the wave's half sit in lanes l ^ 16, l ^ 32, l ^ 48.
+  template <bool FULL>
+  __device__ __forceinline__ void cols16(const f32x4 (&acc)[8][8], int m0, int n0, int M,
+                                         const int* sy, f32x2* red, int wm, int wn,
+                                         int lane) const {
+    const float k1 = scale * 1.44269504088896341f;
+    const int g4 = 4 * (lane >> 4);
+    const int lim = M - m0 - wm * 128 - g4;     // rows 16 i + r >= lim are beyond the vocabulary
+    auto live = [&](int i, int r) { return FULL || 16 * i + r < lim; };
+    float mx[8], sm[8], mk[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      mx[j] = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx[j] = fmaxf(mx[j], live(i, r) ? acc[i][j][r] : -INFINITY);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mx[j] = fmaxf(mx[j], __shfl_xor(mx[j], 16));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      mx[j] = fmaxf(mx[j], __shfl_xor(mx[j], 32));
+      mk[j] = FULL || mx[j] != -INFINITY ? -mx[j] * k1 : 0.0f;
+      sm[j] = 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], k1, mk[j]));
+          sm[j] += live(i, r) ? e : 0.0f;
+        }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sm[j] += __shfl_xor(sm[j], 16);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      sm[j] += __shfl_xor(sm[j], 32);
+      const int c = wn * 128 + j * 16 + (lane & 15);
+      if (lane < 16) red[wm * GBN + c] = f32x2{mx[j] * scale, sm[j]};
+      // target logit: local row o of the target, held here iff 0 <= o < 128 and
+      // bits 2..3 of o equal lane / 16; the register is picked by a select tree
+      // over o's block (bits 4..6) and row (bits 0..1)
+      const int o = sy[c] - wm * 128;
+      float v[32];
+#pragma unroll
+      for (int q = 0; q < 32; ++q) v[q] = acc[q >> 2][j][q & 3];
+      const int idx = ((o >> 4) << 2) | (o & 3);
+#pragma unroll
+      for (int b = 0, w = 16; b < 5; ++b, w >>= 1) {
+        const bool hi = (idx >> b) & 1;
+#pragma unroll
+        for (int q = 0; q < w; ++q) v[q] = hi ? v[2 * q + 1] : v[2 * q];
+      }
+      if ((unsigned)o < 128u && (o & 12) == g4) zy[n0 + c] = v[0] * scale;
+    }
+  }
+
+  __device__ __forceinline__ void tile16(f32x4 (&acc)[8][8], int m0, int n0, int tn, int M,
+                                         int N, uint8_t* smem, int wm, int wn, int lane,
+                                         int tid) const {
+    int* sy = (int*)smem;
+    f32x2* red = (f32x2*)(smem + 1024);
+    sy[tid] = (n0 + tid < N) ? y[n0 + tid] - m0 : -1;
+    __syncthreads();
+    if (m0 + GBM <= M)
+      cols16<true>(acc, m0, n0, M, sy, red, wm, wn, lane);
+    else
+      cols16<false>(acc, m0, n0, M, sy, red, wm, wn, lane);
+    __syncthreads();
+    const int col = n0 + tid;
+    if (col < N) {
+      const f32x2 a = red[tid], b = red[GBN + tid];
+      const float m = fmaxf(a.x, b.x);
+      const float s = (a.y > 0.0f ? a.y * __expf(a.x - m) : 0.0f) +
+                      (b.y > 0.0f ? b.y * __expf(b.x - m) : 0.0f);
+      part[(int64_t)(m0 / GBM) * ld_part + col] = f32x2{m, s};
+    }
+  }
 };
 
 template <typename T>
@@ -1112,23 +1409,87 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
     }
   }
 
+  // per tile row: target column relative to the tile, -lse * log2(e) (-inf on
+  // dead rows, so their exponentials are 0 and G is +0 there), dL/dlogp
+  __device__ __forceinline__ void meta(int m0, int n0, int M, uint8_t* smem, int tid) const {
+    const bool live = m0 + tid < M;
+    ((int*)(smem + EPI_META))[tid] = live ? y[m0 + tid] - col0 - n0 : -1;
+    ((float*)(smem + EPI_META + 1024))[tid] =
+        live ? -lse[m0 + tid] * 1.44269504088896341f : -INFINITY;
+    ((float*)(smem + EPI_META + 2048))[tid] = live ? gs[m0 + tid] : 0.0f;
+  }
+
   __device__ __forceinline__ void tile(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M,
                                        int N, uint8_t* smem, int wm, int wn, int lane,
                                        int tid) const {
-    {
-      const bool live = m0 + tid < M;
-      // target column relative to the tile, -lse * log2(e) (-inf on dead rows, so
-      // their exponentials are 0 and G is +0 there), dL/dlogp
-      ((int*)(smem + EPI_META))[tid] = live ? y[m0 + tid] - col0 - n0 : -1;
-      ((float*)(smem + EPI_META + 1024))[tid] =
-          live ? -lse[m0 + tid] * 1.44269504088896341f : -INFINITY;
-      ((float*)(smem + EPI_META + 2048))[tid] = live ? gs[m0 + tid] : 0.0f;
-    }
+    meta(m0, n0, M, smem, tid);
     __syncthreads();
     const bool full = n0 + GBN <= N;
     pass<0>(acc, full, m0, n0, N, smem, wm, wn, lane, tid);
     __syncthreads();
     pass<1>(acc, full, m0, n0, N, smem, wm, wn, lane, tid);
+  }
+
+  // 16 x 16 accumulator layout: pass h takes blocks i = 4 h .. 4 h + 3 of both
+  // wave rows (the same tile rows as the 32 x 32 layout's pass h); lane l holds
+  // 4 consecutive rows 16 i + 4 (l >> 4) + r of column 16 j + (l & 15).
+  template <bool FULL, int h>
+  __device__ __forceinline__ void stage_pass16(const f32x4 (&acc)[8][8], int n0, int N,
+                                               uint8_t* smem, int wm, int wn, int lane) const {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    const float k1 = scale * 1.44269504088896341f;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int i = 4 * h + ii;
+      const int rt = wm * 128 + 16 * i + 4 * (lane >> 4);      // tile row of r = 0
+      const i32x4 ry = *(const i32x4*)(smem + EPI_META + 4 * rt);
+      const f32x4 rn = *(const f32x4*)(smem + EPI_META + 1024 + 4 * rt);
+      const f32x4 rg = *(const f32x4*)(smem + EPI_META + 2048 + 4 * rt);
+      const int lr = wm * 64 + 16 * ii + 4 * (lane >> 4);       // pass-local row
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int cl = wn * 128 + 16 * j + (lane & 15);
+        float gv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q], k1, rn[q]));
+          gv[q] = fmaf(-rg[q], p, cl == ry[q] ? rg[q] : 0.0f);
+          if constexpr (!FULL) gv[q] = n0 + cl < N ? gv[q] : 0.0f;
+        }
+        const uint32_t p01 = __builtin_bit_cast(
+            uint32_t, __builtin_convertvector(f32x2{gv[0], gv[1]}, bf16x2_t));
+        const uint32_t p23 = __builtin_bit_cast(
+            uint32_t, __builtin_convertvector(f32x2{gv[2], gv[3]}, bf16x2_t));
+        uint8_t* gs_at = smem + EPI_GS + lr * EPI_G_ROW + cl * 2;
+        *(uint16_t*)(gs_at) = (uint16_t)p01;
+        *(uint16_t*)(gs_at + EPI_G_ROW) = (uint16_t)(p01 >> 16);
+        *(uint16_t*)(gs_at + 2 * EPI_G_ROW) = (uint16_t)p23;
+        *(uint16_t*)(gs_at + 3 * EPI_G_ROW) = (uint16_t)(p23 >> 16);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  __device__ __forceinline__ void tile16(f32x4 (&acc)[8][8], int m0, int n0, int tn, int M,
+                                         int N, uint8_t* smem, int wm, int wn, int lane,
+                                         int tid) const {
+    meta(m0, n0, M, smem, tid);
+    __syncthreads();
+    const bool full = n0 + GBN <= N;
+    if (full)
+      stage_pass16<true, 0>(acc, n0, N, smem, wm, wn, lane);
+    else
+      stage_pass16<false, 0>(acc, n0, N, smem, wm, wn, lane);
+    __syncthreads();
+    copy_out<0>(m0, n0, smem, tid);
+    __syncthreads();
+    if (full)
+      stage_pass16<true, 1>(acc, n0, N, smem, wm, wn, lane);
+    else
+      stage_pass16<false, 1>(acc, n0, N, smem, wm, wn, lane);
+    __syncthreads();
+    copy_out<1>(m0, n0, smem, tid);
   }
 
   template <int h>
@@ -1141,26 +1502,29 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
       else
         stage_pass<false, h>(acc, n0, N, smem, wm, wn, lane);
       __syncthreads();
-      // G: 128 rows of 512 bytes; pass rows 0..63 are tile rows 64h + r, rows
-      // 64..127 are tile rows 128 + 64h + (r - 64).  Column-block stage-tiled
-      // addresses: m0 and n0 are multiples of 256, so a thread's block and chunk
-      // are fixed and only the row within the block changes from store to
-      // store.  The loop reads all its LDS chunks before the first store, so the
-      // reads overlap.
-      {
-        const int c16 = tid & 31;
-        __bf16* base = G + (((int64_t)((n0 >> 6) + (c16 >> 3)) * (ldg >> 8) + (m0 >> 8)) << 14);
-        u32x4 v[16];
+      copy_out<h>(m0, n0, smem, tid);
+    }
+  }
+
+  // G: 128 rows of 512 bytes staged in LDS by pass h; pass rows 0..63 are tile
+  // rows 64h + r, rows 64..127 are tile rows 128 + 64h + (r - 64).
+  // Column-block stage-tiled addresses: m0 and n0 are multiples of 256, so a
+  // thread's block and chunk are fixed and only the row within the block
+  // changes from store to store.  The loop reads all its LDS chunks before
+  // the first store, so the reads overlap.
+  template <int h>
+  __device__ __forceinline__ void copy_out(int m0, int n0, uint8_t* smem, int tid) const {
+    const int c16 = tid & 31;
+    __bf16* base = G + (((int64_t)((n0 >> 6) + (c16 >> 3)) * (ldg >> 8) + (m0 >> 8)) << 14);
+    u32x4 v[16];
 #pragma unroll
-        for (int k = 0; k < 16; ++k)
-          v[k] = *(const u32x4*)(smem + EPI_GS + ((tid >> 5) + 8 * k) * EPI_G_ROW + c16 * 16);
+    for (int k = 0; k < 16; ++k)
+      v[k] = *(const u32x4*)(smem + EPI_GS + ((tid >> 5) + 8 * k) * EPI_G_ROW + c16 * 16);
 #pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const int row = (tid >> 5) + 8 * k;
-          const int trow = 64 * h + (row < 64 ? row : row + 64);
-          *(u32x4*)(base + ((trow << 6) + (((c16 & 7) ^ ((trow >> 1) & 7)) << 3))) = v[k];
-        }
-      }
+    for (int k = 0; k < 16; ++k) {
+      const int row = (tid >> 5) + 8 * k;
+      const int trow = 64 * h + (row < 64 ? row : row + 64);
+      *(u32x4*)(base + ((trow << 6) + (((c16 & 7) ^ ((trow >> 1) & 7)) << 3))) = v[k];
     }
   }
 };
@@ -1217,13 +1581,41 @@ struct EpiStore {
       passes<false>(acc, m0, n0, M, st, sr, wave, wm, wn, lane, col_ok);
   }
 
+  // 16 x 16 accumulator layout: pass h stages blocks i = 4 h .. 4 h + 3 of both
+  // wave rows (the same tile rows as the 32 x 32 layout's pass h).  A store
+  // instruction writes 4 rows 4 apart (1 KiB rows, the same banks), so column
+  // c of staged row r sits at c ^ 16 ((r >> 2) & 3): the 4 rows land in 4
+  // distinct groups of 16 banks, and 4 consecutive columns stay together.
+  __device__ __forceinline__ void tile16(f32x4 (&acc)[8][8], int m0, int n0, int tn, int M, int N,
+                                         uint8_t* smem, int wm, int wn, int lane, int tid) const {
+    int* sr = (int*)(smem + EPI_META);
+    if (row_map) sr[tid] = (m0 + tid < M) ? row_map[m0 + tid] : 0;
+    float* st = (float*)smem;
+    const bool col_ok = n0 + 4 * lane < N;
+    const int wave = wm * 2 + wn;
+    auto stage_rows = [&](int h) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int lr = wm * 64 + 16 * ii + 4 * (lane >> 4) + r;
+          const int sw = ((lr >> 2) & 3) << 4;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            st[lr * 256 + ((wn * 128 + 16 * j + (lane & 15)) ^ sw)] = acc[4 * h + ii][j][r];
+        }
+    };
+    if (accumulate)
+      write_out<true, true>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
+    else
+      write_out<false, true>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
+  }
+
   template <bool ACC>
   __device__ __forceinline__ void passes(const f32x16 (&acc)[4][4], int m0, int n0, int M,
                                          float* st, const int* sr, int wave, int wm, int wn,
                                          int lane, bool col_ok) const {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (h) lds_barrier();                        // pass 0's rows have been read
+    auto stage_rows = [&](int h) {
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
@@ -1232,6 +1624,19 @@ struct EpiStore {
 #pragma unroll
           for (int j = 0; j < 4; ++j) st[lr * 256 + acc_col(wn, j, lane)] = acc[2 * h + ii][j][r];
         }
+    };
+    write_out<ACC, false>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
+  }
+
+  // Two passes of 128 staged rows; SWZ: columns stored swizzled as in tile16.
+  template <bool ACC, bool SWZ, class StageRows>
+  __device__ __forceinline__ void write_out(StageRows& stage_rows, int m0, int n0, int M,
+                                            float* st, const int* sr, int wave, int lane,
+                                            bool col_ok) const {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h) lds_barrier();                        // pass 0's rows have been read
+      stage_rows(h);
       lds_barrier();                               // rows staged (and sr written)
       // staged row pr is tile row 64 h + pr (pr < 64) or 128 + 64 h + (pr - 64);
       // wave w writes rows w, w + 4, ..., 16 at a time
@@ -1249,7 +1654,11 @@ struct EpiStore {
         }
         f32x4 v[16];
 #pragma unroll
-        for (int k = 0; k < 16; ++k) v[k] = *(const f32x4*)(st + (wave + 4 * (k0 + k)) * 256 + 4 * lane);
+        for (int k = 0; k < 16; ++k) {
+          const int pr = wave + 4 * (k0 + k);
+          const int c = SWZ ? (4 * lane) ^ (((pr >> 2) & 3) << 4) : 4 * lane;
+          v[k] = *(const f32x4*)(st + pr * 256 + c);
+        }
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
           if constexpr (ACC) v[k] = v[k] + old[k];

@@ -25,6 +25,9 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPer = kScanTile / kScanThreads;   // 16 tokens per thread
 constexpr int kRowPad = 256;             // compacted rows are padded to the GEMM tile
 constexpr int kMergeRows = 64;         // action tokens per merge block
+// stage-pair launches run the 16 x 16 x 32 main loop
+constexpr bool kMf16 = true;
+constexpr bool kMf16Store = false;
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
@@ -622,18 +625,18 @@ void launch_gemm(const GemmShape* g, const Epi* e, int n, int max_tiles, int32_t
     // extents are always whole stage pairs; the callers guarantee it)
     if constexpr (std::is_same<Epi, EpiStore>::value) {
       if (atr && even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, true>), dim3(grid), dim3(GEMM_THREADS), 0,
-                           s, b);
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, true, kMf16Store>), dim3(grid),
+                           dim3(GEMM_THREADS), 0, s, b);
       else if (even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false>), dim3(grid), dim3(GEMM_THREADS), 0,
-                           s, b);
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false, kMf16Store>), dim3(grid),
+                           dim3(GEMM_THREADS), 0, s, b);
       else
         hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
                            0, s, b);
     } else {
       if (even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false>), dim3(grid), dim3(GEMM_THREADS), 0,
-                           s, b);
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false, kMf16>), dim3(grid),
+                           dim3(GEMM_THREADS), 0, s, b);
       else
         hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
                            0, s, b);
