@@ -41,8 +41,12 @@ constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB of stage buff
 // (the store epilogue stages a whole 128 KiB pass below them)
 constexpr int EPI_G_ROW = 528;
 constexpr int EPI_GS = 0;
-constexpr int EPI_META = GEMM_LDS;                          // 131072
-constexpr int EPI_STAGE_LDS = EPI_META + 3 * 1024;          // 134144 B
+// fp32 store epilogue of the 16 x 16 layout: a pass of 128 tile rows staged
+// column-major, 132 floats per column (see EpiStore::tile16)
+constexpr int EPI_COL = 132;
+constexpr int EPI_COLS_LDS = 256 * EPI_COL * 4;             // 135168
+constexpr int EPI_META = EPI_COLS_LDS > GEMM_LDS ? EPI_COLS_LDS : GEMM_LDS;
+constexpr int EPI_STAGE_LDS = EPI_META + 3 * 1024;          // 138240 B
 static_assert(EPI_GS + 128 * EPI_G_ROW <= EPI_META, "G staging below the per-row arrays");
 constexpr int BF16_KERNEL_LDS = EPI_STAGE_LDS > GEMM_LDS ? EPI_STAGE_LDS : GEMM_LDS;
 constexpr int GEMM_THREADS = 256;
@@ -1581,34 +1585,71 @@ struct EpiStore {
       passes<false>(acc, m0, n0, M, st, sr, wave, wm, wn, lane, col_ok);
   }
 
-  // 16 x 16 accumulator layout: pass h stages blocks i = 4 h .. 4 h + 3 of both
-  // wave rows (the same tile rows as the 32 x 32 layout's pass h).  A store
-  // instruction writes 4 rows 4 apart (1 KiB rows, the same banks), so column
-  // c of staged row r sits at c ^ 16 ((r >> 2) & 3): the 4 rows land in 4
-  // distinct groups of 16 banks, and 4 consecutive columns stay together.
+  // 16 x 16 accumulator layout.  Pass h stages blocks i = 4 h .. 4 h + 3 of both
+  // wave rows (the same tile rows as the 32 x 32 layout's pass h), each block
+  // as whole accumulators: a lane's f32x4 (4 consecutive rows of one column)
+  // is one 16-byte LDS write into a column-major staging area (128 rows per
+  // column, padded to EPI_COL floats so that the 16 columns of a write are 16
+  // distinct bank groups).  (Writing the accumulators element by element
+  // makes the register allocator shuffle them through VGPRs inside the main
+  // loop.)  The write-out takes one staged row per wave at a time, lane l
+  // holding columns l, l + 64, l + 128, l + 192: every store instruction
+  // covers 256 consecutive bytes of an output row.
   __device__ __forceinline__ void tile16(f32x4 (&acc)[8][8], int m0, int n0, int tn, int M, int N,
                                          uint8_t* smem, int wm, int wn, int lane, int tid) const {
     int* sr = (int*)(smem + EPI_META);
     if (row_map) sr[tid] = (m0 + tid < M) ? row_map[m0 + tid] : 0;
     float* st = (float*)smem;
-    const bool col_ok = n0 + 4 * lane < N;
+    if (accumulate)
+      out16<true>(acc, m0, n0, M, N, st, sr, wm, wn, lane);
+    else
+      out16<false>(acc, m0, n0, M, N, st, sr, wm, wn, lane);
+  }
+
+  template <bool ACC>
+  __device__ __forceinline__ void out16(const f32x4 (&acc)[8][8], int m0, int n0, int M, int N,
+                                        float* st, const int* sr, int wm, int wn, int lane) const {
     const int wave = wm * 2 + wn;
-    auto stage_rows = [&](int h) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h) lds_barrier();                        // pass 0's rows have been read
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int lr = wm * 64 + 16 * ii + 4 * (lane >> 4) + r;
-          const int sw = ((lr >> 2) & 3) << 4;
+        for (int j = 0; j < 8; ++j)
+          *(f32x4*)(st + (wn * 128 + 16 * j + (lane & 15)) * EPI_COL + wm * 64 + 16 * ii +
+                    4 * (lane >> 4)) = acc[4 * h + ii][j];
+      lds_barrier();                               // rows staged (and sr written)
+      // staged row pr is tile row 64 h + pr (pr < 64) or 128 + 64 h + (pr - 64);
+      // wave w writes rows w, w + 4, ..., 8 rows at a time
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
-            st[lr * 256 + ((wn * 128 + 16 * j + (lane & 15)) ^ sw)] = acc[4 * h + ii][j][r];
+      for (int k0 = 0; k0 < 32; k0 += 8) {
+        float* dst[8];
+        float old[8][4];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int pr = wave + 4 * (k0 + k);
+          const int tr = 64 * h + (pr < 64 ? pr : pr + 64);
+          const int64_t orow = row_map ? (int64_t)sr[tr] : (int64_t)(m0 + tr);
+          dst[k] = m0 + tr < M ? out + orow * ldo + n0 : nullptr;
+          if constexpr (ACC) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+              old[k][m] = dst[k] && n0 + lane + 64 * m < N ? dst[k][lane + 64 * m] : 0.0f;
+          }
         }
-    };
-    if (accumulate)
-      write_out<true, true>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
-    else
-      write_out<false, true>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int pr = wave + 4 * (k0 + k);
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            float v = st[(lane + 64 * m) * EPI_COL + pr];
+            if constexpr (ACC) v += old[k][m];
+            if (dst[k] && n0 + lane + 64 * m < N) dst[k][lane + 64 * m] = v;
+          }
+        }
+      }
+    }
   }
 
   template <bool ACC>
@@ -1625,11 +1666,11 @@ struct EpiStore {
           for (int j = 0; j < 4; ++j) st[lr * 256 + acc_col(wn, j, lane)] = acc[2 * h + ii][j][r];
         }
     };
-    write_out<ACC, false>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
+    write_out<ACC>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
   }
 
-  // Two passes of 128 staged rows; SWZ: columns stored swizzled as in tile16.
-  template <bool ACC, bool SWZ, class StageRows>
+  // Two passes of 128 staged rows of 256 floats.
+  template <bool ACC, class StageRows>
   __device__ __forceinline__ void write_out(StageRows& stage_rows, int m0, int n0, int M,
                                             float* st, const int* sr, int wave, int lane,
                                             bool col_ok) const {
@@ -1655,9 +1696,7 @@ struct EpiStore {
         f32x4 v[16];
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
-          const int pr = wave + 4 * (k0 + k);
-          const int c = SWZ ? (4 * lane) ^ (((pr >> 2) & 3) << 4) : 4 * lane;
-          v[k] = *(const f32x4*)(st + pr * 256 + c);
+          v[k] = *(const f32x4*)(st + (wave + 4 * (k0 + k)) * 256 + 4 * lane);
         }
 #pragma unroll
         for (int k = 0; k < 16; ++k) {

@@ -25,9 +25,10 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPer = kScanTile / kScanThreads;   // 16 tokens per thread
 constexpr int kRowPad = 256;             // compacted rows are padded to the GEMM tile
 constexpr int kMergeRows = 64;         // action tokens per merge block
-// stage-pair launches run the 16 x 16 x 32 main loop
+// stage-pair launches run the 16 x 16 x 32 main loop (the backward's grouped
+// dH + dW launch, which reads A transposed for dW, included)
 constexpr bool kMf16 = true;
-constexpr bool kMf16Store = false;
+constexpr bool kMf16Store = true;
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
@@ -628,8 +629,8 @@ void launch_gemm(const GemmShape* g, const Epi* e, int n, int max_tiles, int32_t
         hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, true, kMf16Store>), dim3(grid),
                            dim3(GEMM_THREADS), 0, s, b);
       else if (even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false, kMf16Store>), dim3(grid),
-                           dim3(GEMM_THREADS), 0, s, b);
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false>), dim3(grid), dim3(GEMM_THREADS), 0,
+                           s, b);
       else
         hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
                            0, s, b);
