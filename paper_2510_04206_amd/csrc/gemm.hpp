@@ -37,8 +37,8 @@ constexpr int STAGE_BYTES = (GBM + GBN) * LDS_ROW;      // 64 KiB
 constexpr int GEMM_LDS = 2 * STAGE_BYTES;               // 128 KiB of stage buffers
 // bf16 logit-gradient epilogue (two passes of 128 tile rows): G rows staged
 // row-major with 528-byte pitch (the two half-waves of a 16-bit store land in
-// different banks); three 256-entry per-row arrays after the stage buffers
-// (the store epilogue stages a whole 128 KiB pass below them)
+// different banks); three 256-entry per-row arrays at EPI_META, above both the
+// stage buffers and the store epilogue's 132 KiB staging of a pass
 constexpr int EPI_G_ROW = 528;
 constexpr int EPI_GS = 0;
 // fp32 store epilogue of the 16 x 16 layout: a pass of 128 tile rows staged
@@ -1515,7 +1515,10 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
   // Column-block stage-tiled addresses: m0 and n0 are multiples of 256, so a
   // thread's block and chunk are fixed and only the row within the block
   // changes from store to store.  The loop reads all its LDS chunks before
-  // the first store, so the reads overlap.
+  // the first store, so the reads overlap.  The stores are non-temporal: G is
+  // read back only by the next launch, and a round of tiles writes as much G
+  // as an XCD's L2 holds, which would otherwise evict the operand panels the
+  // running tiles share.
   template <int h>
   __device__ __forceinline__ void copy_out(int m0, int n0, uint8_t* smem, int tid) const {
     const int c16 = tid & 31;
@@ -1528,7 +1531,8 @@ struct EpiLogitGrad<__bf16> : LogitGradArgs<__bf16> {
     for (int k = 0; k < 16; ++k) {
       const int row = (tid >> 5) + 8 * k;
       const int trow = 64 * h + (row < 64 ? row : row + 64);
-      *(u32x4*)(base + ((trow << 6) + (((c16 & 7) ^ ((trow >> 1) & 7)) << 3))) = v[k];
+      __builtin_nontemporal_store(
+          v[k], (u32x4*)(base + ((trow << 6) + (((c16 & 7) ^ ((trow >> 1) & 7)) << 3))));
     }
   }
 };
