@@ -437,18 +437,30 @@ struct GemmBatch {
 };
 
 // Copy schedule of the 16 x 16 loop, per epilogue (measured on the 32B-shaped
-// workload): MFMA slots between two stage copies, and whether A's copies go
-// before B's.
+// workload): MFMA slots between two stage copies, whether A's copies go before
+// B's, and whether odd rounds of tiles sweep K backwards (a round then starts
+// on the operand chunks the previous round of its XCD read last: 2% faster for
+// the long-K dH + dW tiles, while the forward and recompute gained nothing and
+// their L2 hit rate dropped).
+struct EpiLseCols;
+struct EpiStore;
 template <class Epi>
 struct CopySched {
   static constexpr int spacing = 4;
   static constexpr bool a_first = false;
+  static constexpr bool serpentine = false;
 };
-struct EpiLseCols;
 template <>
 struct CopySched<EpiLseCols> {
   static constexpr int spacing = 6;
   static constexpr bool a_first = false;
+  static constexpr bool serpentine = false;
+};
+template <>
+struct CopySched<EpiStore> {
+  static constexpr int spacing = 4;
+  static constexpr bool a_first = false;
+  static constexpr bool serpentine = true;
 };
 
 // Tile scheduling.  Workgroups are dealt round-robin to the 8 XCDs, so
@@ -590,6 +602,14 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       place(g.a_tiled, g.lda, lda_b, tm, m0, a_off, a_ks);
     }
     place(g.b_tiled, g.ldb, ldb_b, tn, n0, b_off, b_ks);
+    // serpentine K (16 x 16 loop): odd rounds of the problem's tile order copy
+    // the stages last to first
+    if (MF16 && CopySched<Epi>::serpentine && ((L / (32 * nq)) & 1)) {
+      a_off += (int64_t)(nk - 1) * a_ks;
+      b_off += (int64_t)(nk - 1) * b_ks;
+      a_ks = -a_ks;
+      b_ks = -b_ks;
+    }
     const uint8_t* a_base = (const uint8_t*)g.A + a_off;
     const uint8_t* b_base = (const uint8_t*)g.B + b_off;
     // copy q < 8 moves A rows [64 wave + 8 q, +8), q >= 8 the same rows of B;
