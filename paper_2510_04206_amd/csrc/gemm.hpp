@@ -471,7 +471,8 @@ struct CopySched<EpiStore> {
 // all XCDs work on the same few row panels (shared through the Infinity
 // Cache) and each XCD on a compact 8 x 4 block of tiles (shared through its
 // L2), while the workgroups of a queue take its tiles with an atomic counter
-// and balance tiles of unequal length.  Problem 0's tiles come first.
+// and balance tiles of unequal length.  Problem 0's tiles come first.  A
+// workgroup whose queue is empty takes the remaining tiles of the others.
 __device__ __forceinline__ void grouped_tile(int L, int tiles_m, int tiles_n, int group_m,
                                              int& tm, int& tn) {
   const int width = group_m * tiles_n;
@@ -516,14 +517,13 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   static_assert(!MF16 || EVEN, "the 16 x 16 loop runs stage pairs");
   using namespace bf16k;
   __shared__ __attribute__((aligned(16))) uint8_t smem[BF16_KERNEL_LDS];
-  __shared__ int s_tile;
+  __shared__ int s_tile[2];   // claimed tile (-1: none left) and its queue
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int nq = min(8, (int)gridDim.x);
   const int qi = blockIdx.x % nq;
-  int Mp[2], Np[2], Kp[2], tmp[2], tnp[2];
-  QueueShare sh[2];
+  int Mp[2], Np[2], Kp[2], tmp[2], tnp[2], totp[2];
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const GemmShape& gp = bat.g[p];
@@ -534,8 +534,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     Kp[p] = __builtin_amdgcn_readfirstlane(gp.k_dev ? cdiv(*gp.k_dev, KR) * KR : gp.K);
     tmp[p] = cdiv(Mp[p], GBM);
     tnp[p] = cdiv(Np[p], GBN);
-    const int total = (p < bat.n && Mp[p] > 0 && Np[p] > 0) ? tmp[p] * tnp[p] : 0;
-    sh[p] = queue_share(total, qi, nq);
+    totp[p] = (p < bat.n && Mp[p] > 0 && Np[p] > 0) ? tmp[p] * tnp[p] : 0;
   }
 
   // fragment reads: lane l reads row (l & 31) of each 32-row block, chunk
@@ -554,14 +553,38 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   // LDS byte address of the stage buffers
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)smem);
 
+  // Tiles come from the queue of this workgroup's XCD until it runs dry, then
+  // from the other queues in turn (cq: the first queue the next claim tries).
+  // The XCDs do not run at one clock under the power limit (up to 9% apart on
+  // one chip), so without this the slowest XCD's share sets the launch time.
+  // A counter only grows, so a queue found empty stays empty, and a workgroup
+  // leaves after one claim per queue has come back empty.
+  int cq = qi;
   for (;;) {
-    if (wave == 0 && fresh_lane() == 0) s_tile = atomicAdd(bat.queue + qi, 1);
+    if (wave == 0 && fresh_lane() == 0) {
+      int q = cq, k = -1;
+      for (int n = 0; n < nq; ++n) {
+        const int len = queue_share(totp[0], q, nq).len + queue_share(totp[1], q, nq).len;
+        const int c = atomicAdd(bat.queue + q, 1);
+        if (c < len) {
+          k = c;
+          break;
+        }
+        q = q + 1 == nq ? 0 : q + 1;
+      }
+      s_tile[0] = k;
+      s_tile[1] = q;
+    }
     __syncthreads();
     // the same value in every lane: make it a scalar, otherwise every quantity
     // derived from it (loop bounds, the copies' LDS base in M0) is treated as
     // divergent and each copy becomes a waterfall loop
-    const int t = __builtin_amdgcn_readfirstlane(s_tile);
-    if (t >= sh[0].len + sh[1].len) break;
+    const int t = __builtin_amdgcn_readfirstlane(s_tile[0]);
+    if (t < 0) break;
+    cq = __builtin_amdgcn_readfirstlane(s_tile[1]);
+    QueueShare sh[2];
+    sh[0] = queue_share(totp[0], cq, nq);
+    sh[1] = queue_share(totp[1], cq, nq);
     const int p = t < sh[0].len ? 0 : 1;
     const GemmShape g = p ? bat.g[1] : bat.g[0];
     const Epi epi = p ? bat.e[1] : bat.e[0];
@@ -569,7 +592,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     const int N = p ? Np[1] : Np[0];
     const int nk = (p ? Kp[1] : Kp[0]) / SK;
     int tm, tn;
-    const int L = p ? queue_tile(t - sh[0].len, sh[1], qi, nq) : queue_tile(t, sh[0], qi, nq);
+    const int L = p ? queue_tile(t - sh[0].len, sh[1], cq, nq) : queue_tile(t, sh[0], cq, nq);
     if (g.group_cols)
       grouped_tile(L, p ? tnp[1] : tnp[0], p ? tmp[1] : tmp[0], g.group_m, tn, tm);
     else
