@@ -83,10 +83,17 @@ def _run(k, n_dw_rows=8):
     log(f"  sampled dH rows rel fro {e:.2e}")
     assert e <= 2e-2
 
-    # --- dW rows from the oracle's own lse and dL/dlogp
-    rows = np.unique(np.concatenate([rng.choice(w.V, n_dw_rows // 2, replace=False),
+    # --- dW rows from the oracle's own lse and dL/dlogp: every row of two whole
+    # 256-row vocabulary tiles (the first tile of the last vocabulary chunk and the
+    # last tile) plus random rows and sampled targets
+    vc = P.agrl_policy_loss_vocab_chunk(w.T, w.n_act, w.d, w.V, P.AGRL_BF16, None)
+    t_first = ((w.V - 1) // vc) * vc
+    whole = np.concatenate([np.arange(t_first, min(t_first + 256, w.V)),
+                            np.arange(((w.V - 1) // 256) * 256, w.V)])
+    rows = np.unique(np.concatenate([whole, rng.choice(w.V, n_dw_rows // 2, replace=False),
                                      rng.choice(w.token_id[act], n_dw_rows // 2)]))
-    log(f"  oracle dW rows {rows.tolist()}")
+    log(f"  oracle dW rows: {len(rows)} (whole tiles from {t_first} and the last, and "
+        f"{sorted(set(rows.tolist()) - set(whole.tolist()))})")
     ref_rows = oracle.dw_rows(w.H, w.W, w.token_id, w.mask, f["lse"], s["g"], rows)
     got = dW[torch.from_numpy(rows).to(dev)].cpu().numpy()
     ev = rel_fro(got, ref_rows)
