@@ -288,6 +288,10 @@ def main():
     adv_traj = torch.empty(n_traj, dtype=torch.float32, device=dev)
     adv_tok = torch.empty(w.T_g, dtype=torch.float32, device=dev)
     adv_mb = adv_tok[:T]        # the micro-batch is the global stream's first T tokens
+    # member-range scratch of the advantage stages (groups, then tasks)
+    adv_opt = B.agrl_options()
+    ranges = torch.empty(2 * (w.n_group + n_task), dtype=torch.int32, device=dev)
+    adv_opt.adv_ranges = ranges.data_ptr()
 
     K, Wm = args.steps, args.warmup
     events = HipEvents(8 * (K + Wm))
@@ -304,7 +308,7 @@ def main():
         opt.phase_events = events.slice_ptr(8 * i)
         marks[i][0].record()
         B.agrl_task_adv_norm(w.T_g, n_traj, n_task, w.n_group, g_traj, g_mask, traj_task,
-                             traj_group, reward, None, act_count, task_count, task_mean,
+                             traj_group, reward, adv_opt, act_count, task_count, task_mean,
                              task_std, adv_traj, adv_tok)
         marks[i][1].record()
         pl.forward(H, W, token_id, mask, adv_mb, old)

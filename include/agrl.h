@@ -108,6 +108,16 @@ typedef struct {
    * equal (App. A, DAPO's dynamic sampling): its trajectories get advantage 0
    * and are left out of the task statistics.  Needs traj_group. */
   int32_t drop_uniform_groups;
+  /* agrl_task_adv_norm only: NULL, or a device array of 2 * (n_group + n_task)
+   * int32 (2 * n_task without traj_group) that the call uses as scratch.  With
+   * it, the call records the lowest and the highest index of each group's and
+   * each task's trajectories, and each group's and task's wave scans only that
+   * index range instead of all n_traj trajectories: the stages then take work
+   * proportional to the members' spans rather than n_group * n_traj and
+   * n_task * n_traj (trajectories stored segment by segment make every span its
+   * segment's size).  The results are bit-identical either way: the summation
+   * order below does not depend on it.  Calls that overlap must not share it. */
+  int32_t* adv_ranges;
 } agrl_options;
 
 /*

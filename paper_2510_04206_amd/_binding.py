@@ -33,7 +33,7 @@ class agrl_options(ctypes.Structure):
                 ("g_chunk_bytes", ctypes.c_int64), ("phase_events", ctypes.c_void_p),
                 ("kl_beta", ctypes.c_float), ("kl_estimator", ctypes.c_int32),
                 ("ref_logp", ctypes.c_void_p), ("token_weight", ctypes.c_void_p),
-                ("drop_uniform_groups", ctypes.c_int32)]
+                ("drop_uniform_groups", ctypes.c_int32), ("adv_ranges", ctypes.c_void_p)]
 
 
 class AgrlError(RuntimeError):

@@ -10,16 +10,30 @@ from . import _binding as B
 
 def task_adv_norm(traj_id: torch.Tensor, action_mask: torch.Tensor, traj_task: torch.Tensor,
                   traj_group: Optional[torch.Tensor], reward: torch.Tensor, n_task: int,
-                  n_group: int = 0, opt=None, with_tokens: bool = True, stream=None) -> dict:
-    """agrl_task_adv_norm on device tensors; returns the outputs as a dict."""
+                  n_group: int = 0, opt=None, with_tokens: bool = True, stream=None,
+                  member_ranges: bool = True) -> dict:
+    """agrl_task_adv_norm on device tensors; returns the outputs as a dict.
+
+    member_ranges: pass a scratch array as agrl_options.adv_ranges (unless the
+    options already name one), so that each group's and task's wave scans only
+    its members' index span; the results are bit-identical without it."""
     dev = traj_id.device
     T_g, n_traj = traj_id.numel(), traj_task.numel()
+    if member_ranges:
+        o = B.agrl_options(**opt) if isinstance(opt, dict) else (opt or B.agrl_options())
+        if not o.adv_ranges:
+            n_seg = (n_group if traj_group is not None else 0) + n_task
+            scratch = torch.empty(max(2 * n_seg, 1), dtype=torch.int32, device=dev)
+            o.adv_ranges = scratch.data_ptr()
+        opt = o
     out = dict(act_count=torch.empty(n_traj, dtype=torch.int32, device=dev),
                task_count=torch.empty(n_task, dtype=torch.int64, device=dev),
                task_mean=torch.empty(n_task, dtype=torch.float32, device=dev),
                task_std=torch.empty(n_task, dtype=torch.float32, device=dev),
                adv_traj=torch.empty(n_traj, dtype=torch.float32, device=dev),
                adv_tok=torch.empty(T_g, dtype=torch.float32, device=dev) if with_tokens else None)
+    if member_ranges and "scratch" in locals():
+        out["member_ranges"] = scratch     # kept alive with the outputs
     B.agrl_task_adv_norm(T_g, n_traj, n_task, n_group, traj_id, action_mask, traj_task,
                          traj_group, reward, opt, out["act_count"], out["task_count"],
                          out["task_mean"], out["task_std"], out["adv_traj"], out["adv_tok"],

@@ -74,15 +74,62 @@ __global__ __launch_bounds__(256) void count_kernel(int64_t T_g, int32_t n_traj,
   }
 }
 
+// Lowest and highest trajectory index per segment key, one atomic pair per
+// distinct key of the wave: the wave's trajectories are consecutive, so the
+// lowest lane holding a key has its lowest index and the highest lane its highest.
+__device__ __forceinline__ void wave_range(bool valid, int key, int tau, int32_t* range) {
+  const int lane = threadIdx.x & 63;
+  uint64_t pend = __ballot(valid);
+  while (pend) {
+    const int k = __shfl(key, __ffsll((unsigned long long)pend) - 1);
+    const uint64_t m = __ballot(valid && key == k);
+    if (lane == __ffsll((unsigned long long)m) - 1) atomicMin(&range[2 * k], tau);
+    if (lane == 63 - __clzll((unsigned long long)m)) atomicMax(&range[2 * k + 1], tau);
+    pend &= ~m;
+  }
+}
+
 // Zero the per-trajectory counts and check the task / group ids, one launch.
+// With `range` (2 ints per group, then 2 per task, preset to (n_traj, -1)),
+// also record the lowest and the highest index of each group's and each
+// task's members (integer atomics: the result does not depend on the order).
 __global__ void prep_kernel(int32_t n_traj, int32_t n_task, int32_t n_group,
                             const int32_t* traj_task, const int32_t* traj_group,
-                            int32_t* act_count, int* err) {
+                            int32_t* act_count, int32_t* range, int* err) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= n_traj) return;
-  act_count[j] = 0;
-  if (traj_task[j] < 0 || traj_task[j] >= n_task) set_error(err, ERR_TASK_ID);
-  if (traj_group && (traj_group[j] < 0 || traj_group[j] >= n_group)) set_error(err, ERR_GROUP_ID);
+  const bool in = j < n_traj;
+  const int i = in ? traj_task[j] : 0;
+  const int g = in && traj_group ? traj_group[j] : 0;
+  const bool ok_task = in && i >= 0 && i < n_task;
+  const bool ok_group = in && traj_group && g >= 0 && g < n_group;
+  if (in) {
+    act_count[j] = 0;
+    if (!ok_task) set_error(err, ERR_TASK_ID);
+    if (traj_group && !ok_group) set_error(err, ERR_GROUP_ID);
+  }
+  if (range) {
+    if (traj_group) wave_range(ok_group, g, j, range);
+    wave_range(ok_task, i, j, range + 2 * n_group);
+  }
+}
+
+// Preset the member ranges to empty: lowest = n_traj, highest = -1.
+__global__ void range_init_kernel(int32_t n, int32_t n_traj, int32_t* range) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k < n) range[k] = (k & 1) ? -1 : n_traj;
+}
+
+// The trajectories a segment's wave visits: [first, last] of its members when
+// the ranges were recorded, else all of them.  The wave walks them in steps of
+// 64 from first rounded down to a multiple of 64, so that lane l always takes
+// the trajectories tau = l mod 64 in ascending order: the summation order, and
+// so every bit of the result, is the same either way.
+struct Span {
+  int first, last;
+};
+__device__ __forceinline__ Span segment_span(const int32_t* range, int k, int32_t n_traj) {
+  if (!range) return Span{0, n_traj - 1};
+  return Span{range[2 * k], range[2 * k + 1]};
 }
 
 // The fixed combination of a wave's 64 partial sums: acc_l += acc_{l xor o},
@@ -101,14 +148,17 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 // With drop_uniform, a group whose rewards are all equal is marked dropped by a
 // quiet NaN in a_hat (the task stage leaves such trajectories out and gives
 // them advantage 0).
-__device__ void group_wave(int g, int lane, int32_t n_traj, const int32_t* __restrict__ traj_group,
+__device__ void group_wave(int g, int lane, int32_t n_traj, Span sp,
+                           const int32_t* __restrict__ traj_group,
                            const float* __restrict__ reward, int32_t ddof, float eps,
                            int32_t drop_uniform, float* a_hat) {
+  if (sp.last < sp.first) return;      // no members
+  const int t0 = (sp.first & ~63) + lane, end = sp.last + 1;
   float acc = 0.0f;
   int K = 0;
-  for (int base = 0; base < n_traj; base += 64) {
+  for (int base = sp.first & ~63; base < end; base += 64) {
     const int tau = base + lane;
-    const bool mem = tau < n_traj && traj_group[tau] == g;
+    const bool mem = tau < end && traj_group[tau] == g;
     if (mem) acc = acc + reward[tau];
     K += __popcll(__ballot(mem));
   }
@@ -116,7 +166,7 @@ __device__ void group_wave(int g, int lane, int32_t n_traj, const int32_t* __res
   if (drop_uniform) {
     // exact: min and max over the members do not depend on the order
     float lo = INFINITY, hi = -INFINITY;
-    for (int tau = lane; tau < n_traj; tau += 64)
+    for (int tau = t0; tau < end; tau += 64)
       if (traj_group[tau] == g) {
         lo = fminf(lo, reward[tau]);
         hi = fmaxf(hi, reward[tau]);
@@ -126,19 +176,19 @@ __device__ void group_wave(int g, int lane, int32_t n_traj, const int32_t* __res
       hi = fmaxf(hi, __shfl_xor(hi, o));
     }
     if (lo == hi) {
-      for (int tau = lane; tau < n_traj; tau += 64)
+      for (int tau = t0; tau < end; tau += 64)
         if (traj_group[tau] == g) a_hat[tau] = __builtin_nanf("");
       return;
     }
   }
   if (K - ddof <= 0) {
-    for (int tau = lane; tau < n_traj; tau += 64)
+    for (int tau = t0; tau < end; tau += 64)
       if (traj_group[tau] == g) a_hat[tau] = 0.0f;
     return;
   }
   const float mu = butterfly_sum(acc) / (float)K;
   acc = 0.0f;
-  for (int tau = lane; tau < n_traj; tau += 64) {
+  for (int tau = t0; tau < end; tau += 64) {
     if (traj_group[tau] == g) {
       const float dv = reward[tau] - mu;
       acc = acc + dv * dv;
@@ -146,18 +196,19 @@ __device__ void group_wave(int g, int lane, int32_t n_traj, const int32_t* __res
   }
   const float var = butterfly_sum(acc) / (float)(K - ddof);
   const float den = sqrtf(var) + eps;
-  for (int tau = lane; tau < n_traj; tau += 64)
+  for (int tau = t0; tau < end; tau += 64)
     if (traj_group[tau] == g) a_hat[tau] = (reward[tau] - mu) / den;
 }
 
 __global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_traj,
                                                     const int32_t* __restrict__ traj_group,
                                                     const float* __restrict__ reward,
-                                                    int32_t ddof, float eps, int32_t drop_uniform,
-                                                    float* a_hat) {
+                                                    const int32_t* range, int32_t ddof, float eps,
+                                                    int32_t drop_uniform, float* a_hat) {
   const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (g < n_group)
-    group_wave(g, threadIdx.x & 63, n_traj, traj_group, reward, ddof, eps, drop_uniform, a_hat);
+    group_wave(g, threadIdx.x & 63, n_traj, segment_span(range, g, n_traj), traj_group, reward,
+               ddof, eps, drop_uniform, a_hat);
 }
 
 // Task stage: one wave per task; statistics of the token-level set, where
@@ -165,16 +216,18 @@ __global__ __launch_bounds__(256) void group_kernel(int32_t n_group, int32_t n_t
 // src may alias adv_traj: each lane reads its own trajectories before writing them.
 // With drop_uniform, trajectories whose group stage left a NaN mark (dropped
 // groups) are not members of their task's set and get advantage 0.
-__device__ void task_wave(int i, int lane, int32_t n_traj, const int32_t* __restrict__ traj_task,
+__device__ void task_wave(int i, int lane, int32_t n_traj, Span sp,
+                          const int32_t* __restrict__ traj_task,
                           const int32_t* __restrict__ act_count, const float* src, int32_t ddof,
                           float eps, int32_t drop_uniform, int64_t* task_count, float* task_mean,
                           float* task_std, float* adv_traj) {
   auto member = [&](int tau) {
     return traj_task[tau] == i && !(drop_uniform && isnan(src[tau]));
   };
+  const int t0 = (sp.first & ~63) + lane, end = sp.last + 1;   // empty when last < first
   float acc = 0.0f;
   int64_t n_lane = 0;
-  for (int tau = lane; tau < n_traj; tau += 64) {
+  for (int tau = t0; tau < end; tau += 64) {
     if (member(tau)) {
       const int n = act_count[tau];
       n_lane += n;
@@ -183,7 +236,7 @@ __device__ void task_wave(int i, int lane, int32_t n_traj, const int32_t* __rest
   }
   const int64_t N = wave_sum_i64(n_lane);
   if (N == 0) {
-    for (int tau = lane; tau < n_traj; tau += 64)
+    for (int tau = t0; tau < end; tau += 64)
       if (traj_task[tau] == i) adv_traj[tau] = 0.0f;       // dropped ones included
     if (lane == 0) {
       task_count[i] = 0;
@@ -194,7 +247,7 @@ __device__ void task_wave(int i, int lane, int32_t n_traj, const int32_t* __rest
   }
   const float mu = butterfly_sum(acc) / (float)N;
   acc = 0.0f;
-  for (int tau = lane; tau < n_traj; tau += 64) {
+  for (int tau = t0; tau < end; tau += 64) {
     if (member(tau)) {
       const float dv = src[tau] - mu;
       acc = acc + (float)act_count[tau] * (dv * dv);
@@ -203,7 +256,7 @@ __device__ void task_wave(int i, int lane, int32_t n_traj, const int32_t* __rest
   const float q = butterfly_sum(acc);
   const float sigma = (N - ddof > 0) ? sqrtf(q / (float)(N - ddof)) : 0.0f;
   const float den = sigma + eps;
-  for (int tau = lane; tau < n_traj; tau += 64)
+  for (int tau = t0; tau < end; tau += 64)
     if (traj_task[tau] == i) adv_traj[tau] = member(tau) ? (src[tau] - mu) / den : 0.0f;
   if (lane == 0) {
     task_count[i] = N;
@@ -212,17 +265,18 @@ __device__ void task_wave(int i, int lane, int32_t n_traj, const int32_t* __rest
   }
 }
 
-__global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_traj,
+__global__ __launch_bounds__(256) void task_kernel(int32_t n_task, int32_t n_group, int32_t n_traj,
                                                    const int32_t* __restrict__ traj_task,
                                                    const int32_t* __restrict__ act_count,
-                                                   const float* src, int32_t ddof, float eps,
-                                                   int32_t drop_uniform, int64_t* task_count,
-                                                   float* task_mean, float* task_std,
-                                                   float* adv_traj) {
+                                                   const float* src, const int32_t* range,
+                                                   int32_t ddof, float eps, int32_t drop_uniform,
+                                                   int64_t* task_count, float* task_mean,
+                                                   float* task_std, float* adv_traj) {
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i < n_task)
-    task_wave(i, threadIdx.x & 63, n_traj, traj_task, act_count, src, ddof, eps, drop_uniform,
-              task_count, task_mean, task_std, adv_traj);
+    task_wave(i, threadIdx.x & 63, n_traj, segment_span(range, n_group + i, n_traj),
+              traj_task, act_count, src, ddof, eps, drop_uniform, task_count, task_mean,
+              task_std, adv_traj);
 }
 
 // VEC: traj_id, mask and adv_tok are 16-byte aligned and a thread handles 4
@@ -311,9 +365,15 @@ extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, i
   int* err = device_error_ptr();
   if (!err) return hip_status(hipErrorInvalidSymbol);
 
+  // member ranges (optional scratch): groups first, then tasks
+  const int32_t n_group_used = traj_group ? n_group : 0;
+  int32_t* range = n_traj > 0 ? o.adv_ranges : nullptr;
+  if (range && n_group_used + n_task > 0)
+    hipLaunchKernelGGL(range_init_kernel, dim3(cdiv(2 * (n_group_used + n_task), 256)), dim3(256),
+                       0, s, 2 * (n_group_used + n_task), n_traj, range);
   if (n_traj > 0)
     hipLaunchKernelGGL(prep_kernel, dim3(cdiv(n_traj, 256)), dim3(256), 0, s, n_traj, n_task,
-                       n_group, traj_task, traj_group, act_count, err);
+                       n_group_used, traj_task, traj_group, act_count, range, err);
   const bool vec_in = (((uintptr_t)traj_id | (uintptr_t)action_mask) & 15) == 0;
   if (T_g > 0 && n_traj >= 0) {
     const int64_t lanes = cdiv<int64_t>(T_g, kCountPerLane);
@@ -329,10 +389,11 @@ extern "C" int agrl_task_adv_norm(int64_t T_g, int32_t n_traj, int32_t n_task, i
   const int32_t drop = traj_group ? o.drop_uniform_groups : 0;
   if (traj_group && n_group > 0)
     hipLaunchKernelGGL(group_kernel, dim3(cdiv(n_group, 4)), dim3(256), 0, s, n_group, n_traj,
-                       traj_group, reward, ddof, eps, drop, adv_traj);
+                       traj_group, reward, (const int32_t*)range, ddof, eps, drop, adv_traj);
   if (n_task > 0)
-    hipLaunchKernelGGL(task_kernel, dim3(cdiv(n_task, 4)), dim3(256), 0, s, n_task, n_traj,
-                       traj_task, act_count, traj_group ? (const float*)adv_traj : reward, ddof,
+    hipLaunchKernelGGL(task_kernel, dim3(cdiv(n_task, 4)), dim3(256), 0, s, n_task, n_group_used,
+                       n_traj, traj_task, act_count,
+                       traj_group ? (const float*)adv_traj : reward, (const int32_t*)range, ddof,
                        eps, drop, task_count, task_mean, task_std, adv_traj);
   if (adv_tok && T_g > 0) {
     if (vec_in && ((uintptr_t)adv_tok & 15) == 0)

@@ -204,3 +204,26 @@ def test_binding_rejects_host_tensors():
     with pytest.raises(ValueError):
         _binding._ptr(torch.zeros(4))
     assert _binding._ptr(None) is None
+
+
+def test_options_struct_layout_matches_header(tmp_path):
+    """The binding's ctypes agrl_options has the C struct's size and field offsets
+    (a C program built from include/agrl.h with gcc prints them)."""
+    import shutil
+    import subprocess
+    from paper_2510_04206_amd._binding import agrl_options
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not found")
+    names = [f[0] for f in agrl_options._fields_]
+    body = "".join(f'  printf("%s %zu\\n", "{n}", offsetof(agrl_options, {n}));\n' for n in names)
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "agrl.h"\nint main(void) {\n'
+                   '  printf("size %zu\\n", sizeof(agrl_options));\n' + body + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run([gcc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                  check=True).stdout.splitlines())
+    assert int(got["size"]) == ctypes.sizeof(agrl_options)
+    for n in names:
+        assert int(got[n]) == getattr(agrl_options, n).offset, n

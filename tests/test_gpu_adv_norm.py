@@ -16,13 +16,15 @@ pytestmark = pytest.mark.gpu
 KEYS = ("act_count", "task_count", "task_mean", "task_std", "adv_traj", "adv_tok")
 
 
-def _gpu(traj_id, mask, traj_task, traj_group, reward, n_task, n_group, ddof=0, drop=False):
+def _gpu(traj_id, mask, traj_task, traj_group, reward, n_task, n_group, ddof=0, drop=False,
+         ranges=True):
     import paper_2510_04206_amd as P
     dev = "cuda"
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     out = P.task_adv_norm(t(traj_id), t(mask), t(traj_task),
                           None if traj_group is None else t(traj_group), t(reward), n_task,
-                          n_group, opt={"std_ddof": ddof, "drop_uniform_groups": int(drop)})
+                          n_group, opt={"std_ddof": ddof, "drop_uniform_groups": int(drop)},
+                          member_ranges=ranges)
     assert P.agrl_get_device_error() == 0
     return {k: v.cpu().numpy() for k, v in out.items()}
 
@@ -112,3 +114,77 @@ def test_adv_norm_out_of_range_ids_flagged():
                     t(np.array([1.0, 0.0], np.float32)), 1)
     assert P.agrl_get_device_error() & 4
     assert P.agrl_get_device_error() == 0
+
+
+def _shuffled(w, seed):
+    """The same batch with the trajectories renumbered by a random permutation,
+    so that no group or task occupies a contiguous index range."""
+    rng = np.random.default_rng(seed)
+    perm = rng.permutation(w.n_traj).astype(np.int32)      # old index -> new index
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(w.n_traj, dtype=np.int32)
+    tid = w.g_traj_id.copy()
+    tid[tid >= 0] = perm[tid[tid >= 0]]
+    return (tid, w.g_mask, w.traj_task[inv], w.traj_group[inv], w.reward[inv], w.n_task,
+            w.n_group)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_adv_norm_member_ranges_bit_exact(k):
+    """The member-range scans (agrl_options.adv_ranges) and the full scans give
+    the oracle's bits, for trajectories stored segment by segment and for a
+    random renumbering of them, with the group stage and DAPO's drop."""
+    w = gen.config(k, tensors=False)
+    R = w.reward.copy()
+    rng = np.random.default_rng(200 + k)
+    for g in rng.choice(w.n_group, size=max(1, w.n_group // 5), replace=False):
+        R[w.traj_group == g] = R[w.traj_group == g][0]
+    base = (w.g_traj_id, w.g_mask, w.traj_task, w.traj_group, R, w.n_task, w.n_group)
+    for name, args in (("stored by segment", base), ("renumbered", _shuffled(w, 300 + k))):
+        for drop in (False, True):
+            log(f"adv_norm member ranges workload {k} {name} drop={drop}")
+            r = oracle.task_adv_norm(*args, drop_uniform=drop)
+            for ranges in (True, False):
+                _assert_bitwise(_gpu(*args, drop=drop, ranges=ranges), r)
+            tg_none = args[:3] + (None,) + args[4:]
+            if not drop:
+                r0 = oracle.task_adv_norm(*tg_none)
+                _assert_bitwise(_gpu(*tg_none, ranges=True), r0)
+
+
+def test_adv_norm_many_groups():
+    """10^4 groups of 4 over 4 * 10^4 trajectories (a global batch far larger than
+    the workloads'), bit-exact with and without member ranges; both timed."""
+    import paper_2510_04206_amd as P
+    rng = np.random.default_rng(7)
+    n_group, K, n_task = 10000, 4, 50
+    n_traj = n_group * K
+    traj_group = np.repeat(np.arange(n_group, dtype=np.int32), K)
+    traj_task = (traj_group * n_task // n_group).astype(np.int32)
+    reward = rng.random(n_traj, dtype=np.float32)
+    lens = rng.integers(20, 60, n_traj)
+    traj_id = np.repeat(np.arange(n_traj, dtype=np.int32), lens)
+    mask = (rng.random(traj_id.size) < 0.5).astype(np.uint8)
+    args = (traj_id, mask, traj_task, traj_group, reward, n_task, n_group)
+    r = oracle.task_adv_norm(*args)
+    dev = "cuda"
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=dev)
+    T_g = traj_id.size
+    ins = (t(traj_id), t(mask), t(traj_task), t(traj_group), t(reward))
+    outs = (e(n_traj, torch.int32), e(n_task, torch.int64), e(n_task, torch.float32),
+            e(n_task, torch.float32), e(n_traj, torch.float32), e(T_g, torch.float32))
+    scratch = e(2 * (n_group + n_task), torch.int32)
+    for ranges in (True, False):
+        _assert_bitwise(_gpu(*args, ranges=ranges), r)
+        opt = P.agrl_options(adv_ranges=scratch.data_ptr() if ranges else None)
+        call = lambda: P.agrl_task_adv_norm(T_g, n_traj, n_task, n_group, *ins, opt, *outs)
+        call()                                                    # warm-up
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        log(f"adv_norm {n_group} groups, {n_traj} trajectories, T_g={T_g}, "
+            f"member ranges {ranges}: {e0.elapsed_time(e1) / 5 * 1e3:.1f} us per call")
