@@ -506,15 +506,17 @@ __device__ __forceinline__ int queue_tile(int k, const QueueShare& s, int q, int
 }
 
 // EVEN: every problem's K is a multiple of 2 stages (a device-read K is rounded
-// up to one, the operands being zero-padded that far); the stage loop is then
-// unrolled by two and each stage knows its buffer at compile time, so every LDS
-// address of the loop is a base register plus an immediate.  ATR: a problem may
-// read A transposed (GemmShape::a_trans; EVEN launches only).
+// up to one, the operands being zero-padded that far); such launches run the
+// 16 x 16 loop (MF16), whose stage pairs know their buffers at compile time, so
+// every LDS address of the loop is a base register plus an immediate.  Other
+// launches (a hidden size that is not a multiple of 128) run the 32 x 32 loop on
+// row-major operands.  ATR: a problem may read A transposed out of stage-tiled
+// storage (GemmShape::a_trans; 16 x 16 loop only).
 template <class Epi, bool EVEN, bool ATR, bool MF16 = false>
 __global__ void __launch_bounds__(GEMM_THREADS)
     __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_bf16_kernel(GemmBatch<Epi> bat) {
-  static_assert(EVEN || !ATR, "transposed A in the stage-pair loop only");
-  static_assert(!MF16 || EVEN, "the 16 x 16 loop runs stage pairs");
+  static_assert(MF16 == EVEN, "stage-pair launches run the 16 x 16 loop, the others the 32 x 32 loop");
+  static_assert(!ATR || MF16, "transposed A in the 16 x 16 loop only");
   using namespace bf16k;
   __shared__ __attribute__((aligned(16))) uint8_t smem[BF16_KERNEL_LDS];
   __shared__ int s_tile[2];   // claimed tile (-1: none left) and its queue
@@ -664,10 +666,9 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         const int kr = wave * 16 + 2 * b + (ln >> 5);
         const int p = ln & 31;
         const int w = (p >> 2) ^ (kr & 3);
-        // 16 x 16 loop: the 32-byte halves of a window are swapped when bit 3 of
-        // the k-row is set, so lane i holds rows 32 w + 16 hf + 8 (i & 1) .. + 7
-        const int c16 = MF16 ? (w & 1) * 4 + ((((p >> 1) & 1) ^ ((kr >> 3) & 1)) << 1) + (p & 1)
-                             : (w & 1) * 4 + (p & 3);
+        // the 32-byte halves of a window are swapped when bit 3 of the k-row is
+        // set, so lane i holds rows 32 w + 16 hf + 8 (i & 1) .. + 7
+        const int c16 = (w & 1) * 4 + ((((p >> 1) & 1) ^ ((kr >> 3) & 1)) << 1) + (p & 1);
         // (lda <= 2^23 rows: at most 3 * 2^15 blocks of 32 KiB, within 32 bits)
         offa[b] = (uint32_t)((w >> 1) * (uint32_t)((g.lda >> 8) * HALF) + kr * ROW +
                              ((c16 ^ ((kr >> 1) & 7)) << 4));
@@ -883,117 +884,65 @@ __global__ void __launch_bounds__(GEMM_THREADS)
           wait_vmcnt<0>();
         }
         __builtin_amdgcn_s_barrier();
-        // TR: A is read transposed (two half-fragment reads per 32-row block)
-        auto pipeline = [&](auto tr_c) {
-          constexpr bool TR = decltype(tr_c)::value;
-          // transposed A: lane l supplies k-row 8 (l >> 5) + ((l >> 2) & 3) of the
-          // slice and rows 16 ((l >> 4) & 1) + 4 (l & 3) .. + 3 of 32-block i
-          int ta[4];
-          if constexpr (TR) {
-            const int l = fresh_lane();
-            const int q4 = (l >> 2) & 3;
+        // the fragment read paired with MFMA q of a slice (slice kn, buffer
+        // offset off): A blocks first, then B
+        auto frag = [&](int q, int kn, int off, bf16x8 (&fan)[4], bf16x8 (&fbn)[4]) {
+          if (q < 4)
+            fan[q] = *(const bf16x8*)(smem + ra[kn] + off + q * 32 * ROW);
+          else if (q < 8)
+            fbn[q - 4] = *(const bf16x8*)(smem + rb[kn] + off + (q - 4) * 32 * ROW);
+        };
+        bf16x8 fa[2][4], fb[2][4];
   #pragma unroll
-            for (int i = 0; i < 4; ++i)
-              ta[i] = (8 * (l >> 5) + q4) * TR_KROW + (4 * wm + (i ^ q4)) * 64 +
-                      32 * ((l >> 4) & 1) + 8 * (l & 3);
-          }
-          // the fragment read paired with MFMA q of a slice (slice kn, buffer
-          // offset off): A blocks first (two halves each when transposed), then B
-          auto frag = [&](int q, int kn, int off, bf16x8 (&fan)[4], bf16x8 (&fbn)[4]) {
-            if constexpr (TR) {
-              if (q < 8) {
-                const int i = q >> 1;
-                if (q & 1)
-                  fan[i].hi = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW + 4 * TR_KROW);
-                else
-                  fan[i].lo = read_tr(smem + ta[i] + off + kn * 16 * TR_KROW);
-              } else if (q < 12) {
-                fbn[q - 8] = *(const bf16x8*)(smem + rb[kn] + off + (q - 8) * 32 * ROW);
-              }
-            } else {
-              if (q < 4)
-                fan[q] = *(const bf16x8*)(smem + ra[kn] + off + q * 32 * ROW);
-              else if (q < 8)
-                fbn[q - 4] = *(const bf16x8*)(smem + rb[kn] + off + (q - 4) * 32 * ROW);
-            }
-          };
-          bf16x8 fa[2][4], fb[2][4];
-  #pragma unroll
-          for (int q = 0; q < 16; ++q) frag(q, 0, 0, fa[0], fb[0]);
+        for (int q = 0; q < 16; ++q) frag(q, 0, 0, fa[0], fb[0]);
 
-          // P: stage kt's buffer (kt % NB), known at compile time when >= 0
-          auto stage = [&](int kt, auto refill_c, auto more_c, auto par_c) {
-            constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
-            constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
-            constexpr int P = decltype(par_c)::value;
-            using PC = std::integral_constant<int, P>;
-            using PN = std::integral_constant<int, P >= 0 ? (P ^ 1) : -1>;
-            const int pr = P >= 0 ? P : (kt % NB);               // this stage's buffer
-            const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
-            __builtin_amdgcn_sched_barrier(0);
+        // stage kt reads buffer kt % NB
+        auto stage = [&](int kt, auto refill_c, auto more_c) {
+          constexpr bool REFILL = decltype(refill_c)::value;   // copy stage kt + NB
+          constexpr bool MORE = decltype(more_c)::value;       // stage kt + 1 exists
+          const int pr = kt % NB;
+          const int cur_off = pr * HALF, nxt_off = (pr ^ 1) * HALF;
+          __builtin_amdgcn_sched_barrier(0);
   #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-              const int cur = kk & 1, nxt = cur ^ 1;
-              if (kk == KK - 1) {
+          for (int kk = 0; kk < KK; ++kk) {
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk == KK - 1) {
+              if constexpr (MORE) {
+                // stage kt+1 landed (its copies are the only ones in flight)
+                wait_vmcnt<0>();
+              }
+              asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+              __builtin_amdgcn_s_barrier();
+              __builtin_amdgcn_sched_barrier(0);
+            }
+  #pragma unroll
+            for (int q = 0; q < 16; ++q) {
+              const int i = q >> 2, j = q & 3;
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
+                                                                  0, 0, 0);
+              if (kk < KK - 1) {
+                frag(q, kk + 1, cur_off, fa[nxt], fb[nxt]);
                 if constexpr (MORE) {
-                  // stage kt+1 landed (its copies are the only ones in flight)
-                  wait_vmcnt<0>();
+                  const int slot = 16 * (kk + 1) + q;
+                  if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
+                    copy_q(kt + 1, copy_order(slot / CSTRIDE), BUF_RT{}, pr ^ 1);
                 }
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                __builtin_amdgcn_s_barrier();
-                __builtin_amdgcn_sched_barrier(0);
-              }
-  #pragma unroll
-              for (int q = 0; q < 16; ++q) {
-                const int i = q >> 2, j = q & 3;
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
-                                                                    0, 0, 0);
-                if (kk < KK - 1) {
-                  frag(q, kk + 1, cur_off, fa[nxt], fb[nxt]);
-                  if constexpr (MORE) {
-                    const int slot = 16 * (kk + 1) + q;
-                    if (slot % CSTRIDE == 0 && slot / CSTRIDE < NCOPY)
-                      copy_q(kt + 1, copy_order(slot / CSTRIDE), PN{}, pr ^ 1);
-                  }
-                } else {
-                  if constexpr (MORE) frag(q, 0, nxt_off, fa[nxt], fb[nxt]);
-                  if constexpr (REFILL) {
-                    if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), PC{}, pr);
-                  }
+              } else {
+                if constexpr (MORE) frag(q, 0, nxt_off, fa[nxt], fb[nxt]);
+                if constexpr (REFILL) {
+                  if (q % CSTRIDE == 0) copy_q(kt + NB, copy_order(q / CSTRIDE), BUF_RT{}, pr);
                 }
-                __builtin_amdgcn_sched_barrier(0);
               }
+              __builtin_amdgcn_sched_barrier(0);
             }
-          };
-          using T_ = std::true_type;
-          using F_ = std::false_type;
-          if constexpr (EVEN) {
-            // nk even: pairs of stages with buffers 0 and 1, the last pair without
-            // copies of further stages
-            using P0 = std::integral_constant<int, 0>;
-            using P1 = std::integral_constant<int, 1>;
-            int kt = 0;
-            for (; kt + NB < nk; kt += 2) {
-              stage(kt, T_{}, T_{}, P0{});
-              stage(kt + 1, T_{}, T_{}, P1{});
-            }
-            stage(kt, F_{}, T_{}, P0{});
-            stage(kt + 1, F_{}, F_{}, P1{});
-          } else {
-            int kt = 0;
-            for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{}, BUF_RT{});
-            for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{}, BUF_RT{});
-            stage(kt, F_{}, F_{}, BUF_RT{});
           }
         };
-        if constexpr (ATR) {
-          if (atr)
-            pipeline(std::true_type{});
-          else
-            pipeline(std::false_type{});
-        } else {
-          pipeline(std::false_type{});
-        }
+        using T_ = std::true_type;
+        using F_ = std::false_type;
+        int kt = 0;
+        for (; kt + NB < nk; ++kt) stage(kt, T_{}, T_{});
+        for (; kt + 1 < nk; ++kt) stage(kt, F_{}, T_{});
+        stage(kt, F_{}, F_{});
       }
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
       __syncthreads();
@@ -1614,24 +1563,6 @@ struct EpiStore {
       }
   }
 
-  // bf16 kernel: two passes of 128 tile rows staged in LDS as fp32 rows of
-  // 1 KiB, each row then leaving as one 16-byte access per lane (read, added
-  // to and written back when accumulating, the reads of 16 rows in flight at a
-  // time).  Needs out 16-byte aligned and ldo a multiple of 4; N - n0 is a
-  // multiple of 64 (d is), so a lane's 4 columns are all in range or all out.
-  __device__ __forceinline__ void tile(f32x16 (&acc)[4][4], int m0, int n0, int tn, int M, int N,
-                                       uint8_t* smem, int wm, int wn, int lane, int tid) const {
-    int* sr = (int*)(smem + EPI_META);
-    if (row_map) sr[tid] = (m0 + tid < M) ? row_map[m0 + tid] : 0;
-    float* st = (float*)smem;                     // [128][256] staged rows
-    const bool col_ok = n0 + 4 * lane < N;
-    const int wave = wm * 2 + wn;
-    if (accumulate)
-      passes<true>(acc, m0, n0, M, st, sr, wave, wm, wn, lane, col_ok);
-    else
-      passes<false>(acc, m0, n0, M, st, sr, wave, wm, wn, lane, col_ok);
-  }
-
   // 16 x 16 accumulator layout.  Pass h stages blocks i = 4 h .. 4 h + 3 of both
   // wave rows (the same tile rows as the 32 x 32 layout's pass h), each block
   // as whole accumulators: a lane's f32x4 (4 consecutive rows of one column)
@@ -1694,61 +1625,6 @@ struct EpiStore {
             if constexpr (ACC) v += old[k][m];
             if (dst[k] && n0 + lane + 64 * m < N) dst[k][lane + 64 * m] = v;
           }
-        }
-      }
-    }
-  }
-
-  template <bool ACC>
-  __device__ __forceinline__ void passes(const f32x16 (&acc)[4][4], int m0, int n0, int M,
-                                         float* st, const int* sr, int wave, int wm, int wn,
-                                         int lane, bool col_ok) const {
-    auto stage_rows = [&](int h) {
-#pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int lr = wm * 64 + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) st[lr * 256 + acc_col(wn, j, lane)] = acc[2 * h + ii][j][r];
-        }
-    };
-    write_out<ACC>(stage_rows, m0, n0, M, st, sr, wave, lane, col_ok);
-  }
-
-  // Two passes of 128 staged rows of 256 floats.
-  template <bool ACC, class StageRows>
-  __device__ __forceinline__ void write_out(StageRows& stage_rows, int m0, int n0, int M,
-                                            float* st, const int* sr, int wave, int lane,
-                                            bool col_ok) const {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (h) lds_barrier();                        // pass 0's rows have been read
-      stage_rows(h);
-      lds_barrier();                               // rows staged (and sr written)
-      // staged row pr is tile row 64 h + pr (pr < 64) or 128 + 64 h + (pr - 64);
-      // wave w writes rows w, w + 4, ..., 16 at a time
-#pragma unroll
-      for (int k0 = 0; k0 < 32; k0 += 16) {
-        f32x4 old[16];
-        float* dst[16];
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const int pr = wave + 4 * (k0 + k);
-          const int tr = 64 * h + (pr < 64 ? pr : pr + 64);
-          const int64_t orow = row_map ? (int64_t)sr[tr] : (int64_t)(m0 + tr);
-          dst[k] = (m0 + tr < M && col_ok) ? out + orow * ldo + n0 + 4 * lane : nullptr;
-          if constexpr (ACC) old[k] = dst[k] ? *(const f32x4*)dst[k] : f32x4{0, 0, 0, 0};
-        }
-        f32x4 v[16];
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          v[k] = *(const f32x4*)(st + (wave + 4 * (k0 + k)) * 256 + 4 * lane);
-        }
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          if constexpr (ACC) v[k] = v[k] + old[k];
-          if (dst[k]) *(f32x4*)dst[k] = v[k];
         }
       }
     }

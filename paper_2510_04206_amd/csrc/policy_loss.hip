@@ -25,10 +25,6 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPer = kScanTile / kScanThreads;   // 16 tokens per thread
 constexpr int kRowPad = 256;             // compacted rows are padded to the GEMM tile
 constexpr int kMergeRows = 64;         // action tokens per merge block
-// stage-pair launches run the 16 x 16 x 32 main loop (the backward's grouped
-// dH + dW launch, which reads A transposed for dW, included)
-constexpr bool kMf16 = true;
-constexpr bool kMf16Store = true;
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
@@ -622,21 +618,18 @@ void launch_gemm(const GemmShape* g, const Epi* e, int n, int max_tiles, int32_t
     }
     hipLaunchKernelGGL(zero_queue_kernel, dim3(1), dim3(64), 0, s, queue);
     if (ev) hipEventRecord(ev[2 * ph], s);
-    // (transposed A is only built for the backward's dH + dW launch, whose K
-    // extents are always whole stage pairs; the callers guarantee it)
+    // The bf16 store launch is the backward's dH + dW: its operands are
+    // stage-tiled, dW reads G transposed, and both K extents are whole stage
+    // pairs (the vocabulary chunk rounded up to 128, the device-read token count
+    // rounded up in the kernel), so it always runs the 16 x 16 loop.
     if constexpr (std::is_same<Epi, EpiStore>::value) {
-      if (atr && even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, true, kMf16Store>), dim3(grid),
-                           dim3(GEMM_THREADS), 0, s, b);
-      else if (even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false>), dim3(grid), dim3(GEMM_THREADS), 0,
-                           s, b);
-      else
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
-                           0, s, b);
+      (void)atr;
+      (void)even;
+      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, true, true>), dim3(grid), dim3(GEMM_THREADS),
+                         0, s, b);
     } else {
       if (even)
-        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false, kMf16>), dim3(grid),
+        hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true, false, true>), dim3(grid),
                            dim3(GEMM_THREADS), 0, s, b);
       else
         hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false, false>), dim3(grid), dim3(GEMM_THREADS),
