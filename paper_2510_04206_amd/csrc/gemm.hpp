@@ -9,8 +9,10 @@
 // accumulators (half the accumulator traffic per flop: under the board power
 // limit the chip then holds a higher clock).
 // Each K stage moves 128 bytes of every tile row (64 bf16 or 32 fp32) from
-// global memory straight into LDS (no register staging), double-buffered with
-// one barrier per stage.  The 16-byte chunk c of tile row r is stored at chunk
+// global memory straight into LDS (no register staging), double-buffered (one
+// barrier per stage in the 32 x 32 loops; in the 16 x 16 loop a second one in
+// the middle of the stage, so that a stage's copies have until then to land).
+// The 16-byte chunk c of tile row r is stored at chunk
 // c ^ ((r >> 1) & 7): a 128-bit LDS read serves 16 lanes per pass from a
 // 256-byte window (two 128-byte rows), and this places the 16 rows such a pass
 // touches in 16 distinct bank groups.
@@ -300,12 +302,12 @@ __global__ void __launch_bounds__(GEMM_THREADS)
 //   * every MFMA of a slice is paired with at most one LDS fragment read or
 //     one stage copy (sched_barrier keeps that order), so the matrix pipe is
 //     never left waiting behind a burst of memory instructions;
-//   * the barrier of stage kt sits before its last 16-deep slice: by then the
-//     slice's fragments are in registers, stage kt+1 has landed and stage kt's
-//     buffer is free, so the last slice's MFMAs cover the barrier, the reads
-//     of stage kt+1's first slice and the copies of stage kt+2 into the freed
-//     buffer.  __syncthreads() is avoided because it would also wait for the
-//     copies still in flight.
+//   * (32 x 32 loop) the barrier of stage kt sits before its last 16-deep
+//     slice: by then the slice's fragments are in registers, stage kt+1 has
+//     landed and stage kt's buffer is free, so the last slice's MFMAs cover
+//     the barrier, the reads of stage kt+1's first slice and the copies of
+//     stage kt+2 into the freed buffer.  __syncthreads() is avoided because
+//     it would also wait for the copies still in flight.
 namespace bf16k {
 constexpr int SK = 64;                        // k per stage
 constexpr int ROW = SK * 2;                   // bytes per tile row per stage
@@ -366,15 +368,26 @@ __device__ __forceinline__ void copy16(const void* base, uint32_t off, uint32_t 
 
 // 16 x 16 x 32 loop: what rides along with MFMA slot q of a stage (slot
 // q = 16 i + 2 j + kk is block (i, j), slice kk).  Copy c of the stage after
-// next in slot CS c (spread out: a burst of copies stalls issue when the
-// memory pipeline is backed up, and the wave's matrix pipe waits with it; the
-// later a copy, the less time it has to land before the next stage starts);
-// the next stage's A rows i < 7 in place, two slots after row i's last MFMA;
-// its row 7 (into the spare set) and its B fragments in the remaining odd
-// slots below 64, so every read has half a stage or more before its first use.
+// next in slot CS c (even slots, spread over the stage: a burst of copies
+// stalls issue when the memory pipeline is backed up, and the wave's matrix
+// pipe waits with it).  The next stage's fragments are read in the odd slots
+// of the second half only: a wait for the copies of the next stage and a
+// barrier sit before slot 64, so a copy has until the middle of the stage
+// after the one that issued it to land.  A rows 4..6 are replaced in place,
+// two slots after row i's last MFMA; the other odd slots from 65 on carry the
+// 16 B fragments, then A rows 0..3, then row 7 (into the spare set).
 constexpr int MF16_NONE = -1, MF16_COPY = 0, MF16_BREAD = 16, MF16_AREAD = 32;
-__device__ __forceinline__ constexpr bool mf16_arow_slot(int q) {
-  return (q & 1) == 1 && q >= 17 && (q - 17) % 16 < 4 && (q - 17) / 16 < 7;
+constexpr int MF16_MID = 64;   // slot of the mid-stage wait and barrier
+__device__ __forceinline__ constexpr bool mf16_inplace_slot(int q) {
+  return (q & 1) == 1 && q >= 81 && (q - 81) % 16 < 4 && (q - 81) / 16 < 3;
+}
+// rank of odd slot q >= 65 among those not taken by the in-place rows (-1: none)
+__device__ __forceinline__ constexpr int mf16_late_rank(int q) {
+  if ((q & 1) == 0 || q <= MF16_MID || mf16_inplace_slot(q)) return -1;
+  int n = 0;
+  for (int p = MF16_MID + 1; p < q; p += 2)
+    if (!mf16_inplace_slot(p)) ++n;
+  return n;
 }
 // CS: slots between two copies (even, so that copies never share a slot with
 // a fragment read)
@@ -382,16 +395,37 @@ template <int CS>
 __device__ __forceinline__ constexpr int mf16_slot(int q) {
   static_assert(CS % 2 == 0 && 15 * CS < 128, "copy spacing");
   if (q < 16 * CS && q % CS == 0) return MF16_COPY + q / CS;
-  if (mf16_arow_slot(q)) return MF16_AREAD + 2 * ((q - 17) / 16) + ((q - 17) % 16) / 2;
-  if (q == 41 || q == 43) return MF16_AREAD + 14 + (q - 41) / 2;
-  if ((q & 1) == 1 && q < 64) {
-    // the n-th odd slot below 64 not taken above carries B read n
-    int n = 0;
-    for (int p = 1; p < q; p += 2)
-      if (!mf16_arow_slot(p) && p != 41 && p != 43) ++n;
-    return n < 16 ? MF16_BREAD + n : MF16_NONE;
-  }
+  if (mf16_inplace_slot(q)) return MF16_AREAD + 8 + 2 * ((q - 81) / 16) + ((q - 81) % 16) / 2;
+  const int r = mf16_late_rank(q);
+  if (r >= 0 && r < 16) return MF16_BREAD + r;
+  if (r >= 16 && r < 24) return MF16_AREAD + (r - 16);
+  if (r >= 24 && r < 26) return MF16_AREAD + 14 + (r - 24);
   return MF16_NONE;
+}
+// copies a wave issues in a stage before the mid-stage wait
+template <int CS>
+__device__ __forceinline__ constexpr int mf16_early_copies() {
+  return (MF16_MID - 1) / CS + 1 < 16 ? (MF16_MID - 1) / CS + 1 : 16;
+}
+// every fragment of the next stage is read exactly once, after the mid-stage wait
+template <int CS>
+__device__ __forceinline__ constexpr bool mf16_schedule_ok() {
+  int reads[32] = {}, copies[16] = {};
+  for (int q = 0; q < 128; ++q) {
+    const int op = mf16_slot<CS>(q);
+    if (op >= MF16_COPY && op < MF16_COPY + 16) ++copies[op - MF16_COPY];
+    if (op >= MF16_BREAD && op < MF16_AREAD + 16) {
+      if (q <= MF16_MID) return false;
+      ++reads[op - MF16_BREAD];
+    }
+    // an in-place A row only after the last MFMA of that row
+    if (op >= MF16_AREAD && op < MF16_AREAD + 14 && q < 16 * ((op - MF16_AREAD) >> 1) + 17) return false;
+  }
+  for (int n = 0; n < 32; ++n)
+    if (reads[n] != 1) return false;
+  for (int n = 0; n < 16; ++n)
+    if (copies[n] != 1) return false;
+  return true;
 }
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -446,19 +480,19 @@ struct EpiLseCols;
 struct EpiStore;
 template <class Epi>
 struct CopySched {
-  static constexpr int spacing = 4;
-  static constexpr bool a_first = false;
-  static constexpr bool serpentine = false;
-};
-template <>
-struct CopySched<EpiLseCols> {
   static constexpr int spacing = 6;
   static constexpr bool a_first = false;
   static constexpr bool serpentine = false;
 };
 template <>
+struct CopySched<EpiLseCols> {
+  static constexpr int spacing = 8;
+  static constexpr bool a_first = false;
+  static constexpr bool serpentine = false;
+};
+template <>
 struct CopySched<EpiStore> {
-  static constexpr int spacing = 4;
+  static constexpr int spacing = 8;
   static constexpr bool a_first = false;
   static constexpr bool serpentine = true;
 };
@@ -806,9 +840,12 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         auto stage16 = [&](int kt, auto par_c) {
           constexpr int P = decltype(par_c)::value;            // kt % 2
           using PC = std::integral_constant<int, P>;
+          constexpr int CS = CopySched<Epi>::spacing;
+          static_assert(mf16_schedule_ok<CS>(), "16 x 16 slot schedule");
           const int kc = min(kt + 2, nk - 1);                  // stage to copy
-          wait_vmcnt<0>();                                     // stage kt + 1 landed
-          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage kt's fragments
+          // every wave has read its fragments of this stage's buffer, which the
+          // copies below refill
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
           __builtin_amdgcn_s_barrier();
           __builtin_amdgcn_sched_barrier(0);
           // (every index below is a compile-time constant, so that the
@@ -816,7 +853,14 @@ __global__ void __launch_bounds__(GEMM_THREADS)
           static_for<128>([&](auto q_c) {
             constexpr int q = decltype(q_c)::value;
             constexpr int i = q >> 4, j = (q >> 1) & 7, kk = q & 1;
-            constexpr int op = mf16_slot<CopySched<Epi>::spacing>(q);
+            constexpr int op = mf16_slot<CS>(q);
+            if constexpr (q == MF16_MID) {
+              // stage kt + 1 landed: this wave's copies of it are all but the
+              // ones issued so far in this stage, then the other waves'
+              wait_vmcnt<mf16_early_copies<CS>()>();
+              __builtin_amdgcn_s_barrier();
+              __builtin_amdgcn_sched_barrier(0);
+            }
             if constexpr (i == 7 && P == 1)
               acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa7[kk], fb[P][j][kk], acc[i][j],
                                                                   0, 0, 0);
