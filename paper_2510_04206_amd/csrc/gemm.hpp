@@ -467,7 +467,7 @@ struct GemmBatch {
   GemmShape g[2];
   Epi e[2];
   int32_t n;          // number of problems
-  int32_t* queue;     // 8 tile counters, zero at launch
+  int32_t* queue;     // 8 tile counters, then 8 finished-tile counters, zero at launch
 };
 
 // Copy schedule of the 16 x 16 loop, per epilogue (measured on the 32B-shaped
@@ -483,19 +483,24 @@ struct CopySched {
   static constexpr int spacing = 6;
   static constexpr bool a_first = false;
   static constexpr bool serpentine = false;
+  static constexpr bool round_sync = false;
 };
 template <>
 struct CopySched<EpiLseCols> {
   static constexpr int spacing = 8;
   static constexpr bool a_first = false;
   static constexpr bool serpentine = false;
+  static constexpr bool round_sync = false;
 };
 template <>
 struct CopySched<EpiStore> {
   static constexpr int spacing = 8;
   static constexpr bool a_first = false;
   static constexpr bool serpentine = true;
+  static constexpr bool round_sync = true;
 };
+constexpr int ROUND_SLACK = 2;   // tiles of the earlier rounds that may still run
+constexpr int ROUND_SPIN = 32;   // polls of the finished-tile counter (~0.3 us apart)
 
 // Tile scheduling.  Workgroups are dealt round-robin to the 8 XCDs, so
 // workgroup b serves queue b % nq (nq = 8, fewer for a small grid).  A
@@ -595,9 +600,10 @@ __global__ void __launch_bounds__(GEMM_THREADS)
   // one chip), so without this the slowest XCD's share sets the launch time.
   // A counter only grows, so a queue found empty stays empty, and a workgroup
   // leaves after one claim per queue has come back empty.
-  int cq = qi;
+  int cq = qi, done_q = -1;
   for (;;) {
     if (wave == 0 && fresh_lane() == 0) {
+      if (CopySched<Epi>::round_sync && done_q >= 0) atomicAdd(bat.queue + 8 + done_q, 1);
       int q = cq, k = -1;
       for (int n = 0; n < nq; ++n) {
         const int len = queue_share(totp[0], q, nq).len + queue_share(totp[1], q, nq).len;
@@ -607,6 +613,24 @@ __global__ void __launch_bounds__(GEMM_THREADS)
           break;
         }
         q = q + 1 == nq ? 0 : q + 1;
+      }
+      if constexpr (CopySched<Epi>::round_sync) {
+        // a tile of a full round starts once all but a few tiles of the queue's
+        // earlier rounds of the same problem have finished (bounded wait)
+        if (k >= 0) {
+          const QueueShare s0 = queue_share(totp[0], q, nq), s1 = queue_share(totp[1], q, nq);
+          int target = 0;
+          if (k < s0.full)
+            target = k & ~31;
+          else if (k >= s0.len && k - s0.len < s1.full)
+            target = s0.full + ((k - s0.len) & ~31);
+          target -= ROUND_SLACK;
+          for (int it = 0; it < ROUND_SPIN && target > 0 &&
+                           __hip_atomic_load(bat.queue + 8 + q, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT) < target;
+               ++it)
+            __builtin_amdgcn_s_sleep(8);
+        }
       }
       s_tile[0] = k;
       s_tile[1] = q;
@@ -618,6 +642,7 @@ __global__ void __launch_bounds__(GEMM_THREADS)
     const int t = __builtin_amdgcn_readfirstlane(s_tile[0]);
     if (t < 0) break;
     cq = __builtin_amdgcn_readfirstlane(s_tile[1]);
+    done_q = cq;
     QueueShare sh[2];
     sh[0] = queue_share(totp[0], cq, nq);
     sh[1] = queue_share(totp[1], cq, nq);

@@ -588,7 +588,7 @@ int validate(const char* fn, int64_t T, int64_t max_act, int32_t d, int32_t V, i
 enum Phase { PH_FWD = 0, PH_RECOMPUTE = 1, PH_DW = 2, PH_DH = 3 };
 
 __global__ void zero_queue_kernel(int32_t* q) {
-  if (threadIdx.x < 8) q[threadIdx.x] = 0;
+  if (threadIdx.x < 16) q[threadIdx.x] = 0;
 }
 
 // Launch n (1 or 2) independent products.  bf16: one persistent launch of the
