@@ -783,9 +783,10 @@ __global__ void __launch_bounds__(GEMM_THREADS)
       // fragments are in registers before it starts: fa[i][kk] (A, replaced in
       // place by the next stage's row i once row i's MFMAs are issued; row 7 of
       // odd stages lives in fa7) and fb[P][j][kk] (B, two sets by stage parity).
-      // One barrier per stage, at its start: the next stage has landed and
-      // every wave is done reading this stage's buffer, which the copies of
-      // the stage after next then refill.
+      // Two barriers per stage: at its start every wave is done reading this
+      // stage's buffer, which the copies of the stage after next then refill;
+      // before slot 64 the next stage has landed, and its fragments are read
+      // in the second half.
       // one accumulator set and one epilogue for both operand modes (TR: A
       // read transposed); only the main loop is instantiated per mode
       f32x4 acc[8][8];
