@@ -389,33 +389,46 @@ __device__ __forceinline__ constexpr int mf16_late_rank(int q) {
     if (!mf16_inplace_slot(p)) ++n;
   return n;
 }
+// SPLIT (transposed A, whose fragments take two LDS reads each): the B
+// fragments come first, in the odd slots 33..63 behind a wait for the next
+// stage's B copies (a stage issues B's copies before A's) at slot 32, so that
+// the second half carries only A's reads.
+constexpr int MF16_MID_B = 32;   // slot of the wait for B's copies (SPLIT)
 // CS: slots between two copies (even, so that copies never share a slot with
 // a fragment read)
-template <int CS>
+template <int CS, bool SPLIT = false>
 __device__ __forceinline__ constexpr int mf16_slot(int q) {
   static_assert(CS % 2 == 0 && 15 * CS < 128, "copy spacing");
   if (q < 16 * CS && q % CS == 0) return MF16_COPY + q / CS;
   if (mf16_inplace_slot(q)) return MF16_AREAD + 8 + 2 * ((q - 81) / 16) + ((q - 81) % 16) / 2;
+  if (SPLIT) {
+    if ((q & 1) == 1 && q > MF16_MID_B && q < MF16_MID) return MF16_BREAD + (q - MF16_MID_B) / 2;
+    const int r = mf16_late_rank(q);
+    if (r >= 0 && r < 8) return MF16_AREAD + r;
+    if (r >= 8 && r < 10) return MF16_AREAD + 14 + (r - 8);
+    return MF16_NONE;
+  }
   const int r = mf16_late_rank(q);
   if (r >= 0 && r < 16) return MF16_BREAD + r;
   if (r >= 16 && r < 24) return MF16_AREAD + (r - 16);
   if (r >= 24 && r < 26) return MF16_AREAD + 14 + (r - 24);
   return MF16_NONE;
 }
-// copies a wave issues in a stage before the mid-stage wait
+// copies a wave issues in a stage before slot q
 template <int CS>
-__device__ __forceinline__ constexpr int mf16_early_copies() {
-  return (MF16_MID - 1) / CS + 1 < 16 ? (MF16_MID - 1) / CS + 1 : 16;
+__device__ __forceinline__ constexpr int mf16_copies_before(int q) {
+  return (q - 1) / CS + 1 < 16 ? (q - 1) / CS + 1 : 16;
 }
-// every fragment of the next stage is read exactly once, after the mid-stage wait
-template <int CS>
+// every fragment of the next stage is read exactly once, after the wait for
+// its copies
+template <int CS, bool SPLIT = false>
 __device__ __forceinline__ constexpr bool mf16_schedule_ok() {
   int reads[32] = {}, copies[16] = {};
   for (int q = 0; q < 128; ++q) {
-    const int op = mf16_slot<CS>(q);
+    const int op = mf16_slot<CS, SPLIT>(q);
     if (op >= MF16_COPY && op < MF16_COPY + 16) ++copies[op - MF16_COPY];
     if (op >= MF16_BREAD && op < MF16_AREAD + 16) {
-      if (q <= MF16_MID) return false;
+      if (q <= (SPLIT && op < MF16_AREAD ? MF16_MID_B : MF16_MID)) return false;
       ++reads[op - MF16_BREAD];
     }
     // an in-place A row only after the last MFMA of that row
@@ -840,11 +853,13 @@ __global__ void __launch_bounds__(GEMM_THREADS)
         auto rd_b = [&](int j, int kk, int buf) {
           return *(const bf16x8*)(smem + rb16[kk] + buf * HALF + j * 16 * ROW);
         };
-        // stages 0 and 1 whole
+        // stages 0 and 1 whole (stage 1 in the loop's copy order, which the
+        // first stage's waits assume)
 #pragma unroll
         for (int q = 0; q < NCOPY; ++q) copy_q(0, q, std::integral_constant<int, 0>{}, 0);
 #pragma unroll
-        for (int q = 0; q < NCOPY; ++q) copy_q(1, q, std::integral_constant<int, 1>{}, 1);
+        for (int q = 0; q < NCOPY; ++q)
+          copy_q(1, CopySched<Epi>::a_first ? q : copy_order(q), std::integral_constant<int, 1>{}, 1);
         wait_vmcnt<NCOPY>();        // stage 0 landed (stage pairs: nk >= 2)
         __builtin_amdgcn_s_barrier();
         using P0 = std::integral_constant<int, 0>;
@@ -867,7 +882,9 @@ __global__ void __launch_bounds__(GEMM_THREADS)
           constexpr int P = decltype(par_c)::value;            // kt % 2
           using PC = std::integral_constant<int, P>;
           constexpr int CS = CopySched<Epi>::spacing;
-          static_assert(mf16_schedule_ok<CS>(), "16 x 16 slot schedule");
+          constexpr bool SPLIT = TR;
+          static_assert(mf16_schedule_ok<CS, SPLIT>(), "16 x 16 slot schedule");
+          static_assert(!SPLIT || !CopySched<Epi>::a_first, "B's copies go first");
           const int kc = min(kt + 2, nk - 1);                  // stage to copy
           // every wave has read its fragments of this stage's buffer, which the
           // copies below refill
@@ -879,11 +896,18 @@ __global__ void __launch_bounds__(GEMM_THREADS)
           static_for<128>([&](auto q_c) {
             constexpr int q = decltype(q_c)::value;
             constexpr int i = q >> 4, j = (q >> 1) & 7, kk = q & 1;
-            constexpr int op = mf16_slot<CS>(q);
+            constexpr int op = mf16_slot<CS, SPLIT>(q);
+            if constexpr (SPLIT && q == MF16_MID_B) {
+              // stage kt + 1's B half landed: this wave's first 8 copies of the
+              // previous stage, before its 8 A copies and this stage's copies
+              wait_vmcnt<8 + mf16_copies_before<CS>(MF16_MID_B)>();
+              __builtin_amdgcn_s_barrier();
+              __builtin_amdgcn_sched_barrier(0);
+            }
             if constexpr (q == MF16_MID) {
               // stage kt + 1 landed: this wave's copies of it are all but the
               // ones issued so far in this stage, then the other waves'
-              wait_vmcnt<mf16_early_copies<CS>()>();
+              wait_vmcnt<mf16_copies_before<CS>(MF16_MID)>();
               __builtin_amdgcn_s_barrier();
               __builtin_amdgcn_sched_barrier(0);
             }
